@@ -1,0 +1,141 @@
+"""Pins for the oracle's masks, pair counts and cost model against what the
+paper fixes: the mask prose of Sec. 3.3 (tables in tests/golden/masks.txt),
+the interaction counts of App. C (Eqs. cost-pre, cost-step) and Eq. 4, the
+0.87x the paper prints for its large-context approximation, the monotonicity
+and T-fold ceiling it proves, and Theorem 1 of App. A."""
+import itertools
+import os
+
+import numpy as np
+import pytest
+
+from oracle import cost as oc
+from oracle import graph as og
+from oracle import masks as om
+
+ST, LT, X, R = om.ST, om.LT, om.X, om.R
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def read_golden_masks():
+    tables = {}
+    for line in open(os.path.join(GOLDEN, "masks.txt")):
+        line = line.split("#")[0].strip()
+        if not line:
+            continue
+        name, _row, *bits = line.split()
+        tables.setdefault(name, []).append([b == "1" for b in bits])
+    return tables
+
+
+def read_golden_kv(fname):
+    out = {}
+    for line in open(os.path.join(GOLDEN, fname)):
+        line = line.split("#")[0].strip()
+        if line:
+            k, v = (t.strip() for t in line.split("="))
+            out[k] = float(v)
+    return out
+
+
+@pytest.mark.parametrize("preset", ["paper", "perref", "isolated", "dense"])
+def test_mask_tables_match_prose(preset):
+    kinds = [ST, LT, X, R, R]
+    assert om.PRESETS[preset](kinds) == read_golden_masks()[preset]
+
+
+def test_pair_counts_match_cost_equations():
+    """PAPER mask: prefill pairs = (N_R+N_ST)^2, step pairs = S (N_R+S);
+    dense over [LT, X, R]: (N_R+S)^2; PAPER minus ISOLATED prefill = Eq. 4."""
+    for n_st, n_lt, n_x, refs in [(64, 512, 4096, [4096]), (64, 512, 4096, [4096] * 5),
+                                  (7, 33, 100, [17, 5, 64]), (1, 1, 1, [1])]:
+        kinds = [ST, LT, X] + [R] * len(refs)
+        lens = [n_st, n_lt, n_x] + refs
+        n_r, s = sum(refs), n_lt + n_x
+        vp = om.paper_mask(kinds)
+        assert oc.visible_pairs(kinds, lens, vp, "static") == oc.c_pre(n_r, n_st)
+        assert oc.visible_pairs(kinds, lens, vp, "live") == oc.c_step(n_r, s)
+        base_k, base_l = kinds[1:], lens[1:]
+        assert oc.visible_pairs(base_k, base_l, om.dense_mask(base_k), "all") * 40 == oc.c_full(n_r, s, 40)
+        vi = om.isolated_mask(kinds)
+        assert (oc.visible_pairs(kinds, lens, vp, "static") - oc.visible_pairs(kinds, lens, vi, "static")
+                == oc.anchor_overhead(n_r, n_st))
+        # per-reference workload mask: live rows see everything, refs see own block + anchors
+        vr = om.perref_mask(kinds)
+        assert oc.visible_pairs(kinds, lens, vr, "live") == s * (n_st + s + n_r)
+        assert oc.visible_pairs(kinds, lens, vr, "static") == n_st ** 2 + sum(n * (n + n_st) for n in refs)
+
+
+def test_printed_large_context_approximation():
+    g = read_golden_kv("cost_model.txt")
+    val = oc.speedup_large_context(g["approx_one_ref_NR"], g["approx_one_ref_S"], g["approx_one_ref_T"])
+    assert round(val, 2) == g["approx_one_ref_speedup_2dp"]
+    # the exact model, keeping N_ST, is well above it at one reference (App. C, last paragraph)
+    assert oc.speedup(4096, 64, 4608, 40) > 1.8
+
+
+def test_speedup_equation_consistency():
+    # Eq. speedup written as C_full / C_ours with hand-expanded terms
+    for n_r, n_st, s, T in [(4096, 64, 4608, 40), (20480, 64, 4608, 40), (1, 0, 1, 3)]:
+        expect = T * (n_r + s) ** 2 / ((n_r + n_st) ** 2 + T * s * (n_r + s))
+        assert oc.speedup(n_r, n_st, s, T) == pytest.approx(expect, rel=1e-15)
+
+
+def test_monotone_and_below_T():
+    """App. C: R'(N_R) > 0 and R(N_R) < T for T > 2 and 0 <= N_ST <= S."""
+    for T, s, n_st in [(3, 100, 0), (40, 4608, 64), (40, 4608, 4608), (10, 50, 25)]:
+        xs = np.unique(np.round(np.geomspace(1, 1e7, 400)).astype(np.int64))
+        ys = [oc.speedup(int(n), n_st, s, T) for n in xs]
+        assert all(b > a for a, b in zip(ys, ys[1:]))
+        assert all(y < T for y in ys)
+
+
+def test_crossover_scale():
+    """App. C: precompute and repeated live cost cross near N_R ~ T S."""
+    T, s, n_st = 40, 4608, 64
+    n = next(n for n in range(1, 10 ** 7, 64) if oc.c_pre(n, n_st) >= T * oc.c_step(n, s))
+    assert 0.8 * T * s < n < 1.3 * T * s
+
+
+def test_theorem1_exhaustive():
+    """App. A, Theorem 1: on blocks {LT, X, R} with LT reading X (M[X, LT] = 1)
+    and L >= 2, no layer-shared mask is both StructCacheable(R) and
+    LiveTextReachable(R).  Checked over all 2^9 masks, L = 2, 3, 4."""
+    LTb, Xb, Rb = 0, 1, 2
+    found_each = [False, False]
+    for bits in itertools.product([False, True], repeat=9):
+        vis = [list(bits[0:3]), list(bits[3:6]), list(bits[6:9])]
+        if not vis[LTb][Xb]:
+            continue
+        for L in (2, 3, 4):
+            c = og.struct_cacheable(vis, [Xb], [Rb], L)
+            r = og.live_text_reachable(vis, [LTb], [Rb], L)
+            assert not (c and r)
+            found_each[0] |= c
+            found_each[1] |= r
+    assert all(found_each)  # both properties occur separately
+
+
+def test_anchor_masks_escape_theorem_domain():
+    """Sec. 3.3 / App. A closing paragraph: with ST added, the instruction
+    reaches R through ST while R stays structurally cacheable; the live-text
+    mask of Sec. 3.2 reaches R from LT but loses cacheability."""
+    kinds = [ST, LT, X, R, R]
+    for p in ("paper", "perref"):
+        vis = om.PRESETS[p](kinds)
+        assert og.struct_cacheable(vis, [2], [3, 4], 4)
+        assert not og.live_text_reachable(vis, [1], [3, 4], 4)
+        assert any((rb, 1) in og.reachable_from(vis, 0, 0, 4) for rb in (3, 4))   # ST -> R
+    vis = om.live_text_mask(kinds)
+    assert not og.struct_cacheable(vis, [2], [3, 4], 3)
+    assert og.live_text_reachable(vis, [1], [3, 4], 3)
+    # Eq. 3 timing: X^(0) -> LT^(1) -> R^(2); not earlier
+    reach = og.reachable_from(vis, 2, 0, 3)
+    assert (1, 1) in reach and (3, 1) not in reach and (3, 2) in reach
+
+
+def test_cached_segments():
+    kinds = [ST, LT, X, R, R]
+    assert om.cached_segments(kinds, om.paper_mask(kinds)) == [3, 4]
+    assert om.cached_segments(kinds, om.perref_mask(kinds)) == [0, 3, 4]
+    assert om.cached_segments(kinds, om.isolated_mask(kinds)) == [3, 4]
