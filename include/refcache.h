@@ -1,0 +1,185 @@
+/*
+ * refcache.h -- C ABI of librefcache: block-masked multi-head attention for
+ * exact reference caching in in-context diffusion transformers
+ * (arXiv 2608.21229, "Anchoring Instruction Outside Mask").
+ *
+ * The sequence is a list of segments in order (Sec. 3.1, Eq. 1; Sec. 3.3):
+ *   ST  static text anchors   (kind RC_SEG_ANCHOR)
+ *   LT  live text             (kind RC_SEG_TEXT)
+ *   X   denoising target      (kind RC_SEG_TARGET)
+ *   R^k reference k           (kind RC_SEG_REF)
+ * ST and R are the static subgraph: fixed for a whole request.  LT and X are
+ * live: their Q/K/V change at every denoising step.
+ *
+ * Three entry points (App. C, derivation paragraph):
+ *   rc_ref_kv_prefill         once per request and layer: the static rows
+ *                             attend within the static subgraph, and the K/V
+ *                             of every static segment that a live query reads
+ *                             are written to the reference K/V cache (Eq. 2).
+ *   rc_step_masked_attention  every denoising step: the live rows attend to
+ *                             fresh LT/X K/V plus the cached K/V.
+ *   rc_full_attention         the recompute baseline: all rows over the whole
+ *                             sequence under any mask (dense over [LT,X,R] is
+ *                             the paper's full-attention Base).
+ *
+ * Common conventions
+ *   Element type   bf16 for Q, K, V, O and the cache (passed as raw bits);
+ *                  fp32 for LSE and workspace.  Arithmetic: bf16 products,
+ *                  fp32 accumulation and softmax, O rounded to bf16 (RNE).
+ *   Token layout   Q/K/V are [B, N, H, D] with D contiguous and head stride D;
+ *                  `tok_stride` (elements, >= H*D, multiple of 8) separates
+ *                  consecutive tokens so views into a fused QKV buffer work;
+ *                  batch stride is N * tok_stride.  O is contiguous
+ *                  [B, N, H, D].  LSE is contiguous [B, H, N] (natural log).
+ *   Cache layout   [B, H, N_cached, D] contiguous, one buffer for K and one
+ *                  for V; rows are the cached segments in sequence order.
+ *   Pointers       device pointers, 16-byte aligned; `stream` is a
+ *                  hipStream_t passed as void* (NULL = default stream).
+ *   Ownership      the caller allocates every buffer; the library allocates
+ *                  nothing and keeps no device state.  An rc_layout is read
+ *                  only during the call.
+ *   Asynchrony     calls enqueue kernels on `stream` and return without
+ *                  synchronising.  Results are deterministic: fixed
+ *                  reduction order, no atomics.
+ *   Errors         every function validates all arguments before any HIP
+ *                  call and returns an rc_status; on error nothing is
+ *                  launched and rc_last_error() (thread-local) describes it.
+ *   head_dim       D in {64, 128}.
+ */
+#ifndef REFCACHE_H
+#define REFCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RC_MAX_SEGMENTS 32
+
+typedef enum {
+  RC_OK = 0,
+  RC_ERR_ARG = -1,                 /* null/misaligned pointer, bad size or stride */
+  RC_ERR_UNSUPPORTED = -2,         /* head_dim not 64/128, schedule too fragmented */
+  RC_ERR_MASK_NOT_CACHEABLE = -3,  /* a static query reads a live segment */
+  RC_ERR_WORKSPACE = -4,           /* split-KV workspace missing or too small */
+  RC_ERR_HIP = -5                  /* a HIP launch failed */
+} rc_status;
+
+typedef enum {
+  RC_SEG_ANCHOR = 0,  /* ST: static text anchors, timestep fixed at 0 (Sec. 3.3) */
+  RC_SEG_TEXT = 1,    /* LT: live text (Sec. 3.1) */
+  RC_SEG_TARGET = 2,  /* X_t: denoising target (Sec. 3.1) */
+  RC_SEG_REF = 3      /* R^(k): one reference image's tokens (Sec. 3.1, Eq. 1) */
+} rc_seg_kind;
+
+typedef enum {
+  /* Sec. 3.3: ST <-> R see each other (all references form one R block);
+   * neither reads LT or X; LT and X read LT, X and R but not ST. */
+  RC_MASK_PAPER = 0,
+  /* Per-reference anchored mask of the synthetic workloads: R^(k) reads
+   * ST and itself, ST reads ST, LT and X read every segment. */
+  RC_MASK_PERREF = 1,
+  /* Prior-work isolated cache (Sec. 1, Sec. 2): R reads R, LT and X read
+   * LT, X, R; anchor segments are detached (no keys, read by nobody). */
+  RC_MASK_ISOLATED = 2,
+  /* Full attention: every segment reads every segment (App. C Base). */
+  RC_MASK_DENSE = 3
+} rc_mask_preset;
+
+typedef enum { RC_ENTRY_PREFILL = 0, RC_ENTRY_STEP = 1, RC_ENTRY_FULL = 2 } rc_entry;
+
+typedef enum {
+  RC_ROWS_STATIC = 0,  /* tokens of ST and R segments */
+  RC_ROWS_LIVE = 1,    /* tokens of LT and X segments */
+  RC_ROWS_CACHED = 2,  /* tokens of the cached segments */
+  RC_ROWS_ALL = 3      /* all tokens */
+} rc_rows_kind;
+
+typedef struct {
+  int32_t kind;  /* rc_seg_kind */
+  int32_t len;   /* tokens, >= 1 */
+} rc_segment;
+
+/* Segment table + segment-level block mask.  visible[q] bit k set means the
+ * tokens of query segment q attend to the tokens of key segment k (query
+ * first; App. A writes the transpose, M[b',b] = 1 for "b attends b'"). */
+typedef struct {
+  int32_t n_seg;
+  rc_segment seg[RC_MAX_SEGMENTS];
+  uint32_t visible[RC_MAX_SEGMENTS];
+} rc_layout;
+
+/* Fill L->visible from the segment kinds for one rc_mask_preset.  n_seg and
+ * seg[] must already be set.  RC_ERR_ARG on a bad table or preset. */
+rc_status rc_layout_preset(rc_layout* L, int32_t preset);
+
+/* Check a layout for one entry (rc_entry): 1 <= n_seg <= 32, every len >= 1,
+ * known kinds, no visible bit beyond n_seg; for PREFILL and STEP also the
+ * caching condition (no static query segment reads LT or X; App. A,
+ * StructCacheable for a layer-shared mask) -> RC_ERR_MASK_NOT_CACHEABLE. */
+rc_status rc_layout_validate(const rc_layout* L, int32_t entry);
+
+/* Visible query-key pairs per (batch, head) for the rows of `entry`
+ * (App. C: one unit per query-key interaction).  Useful FLOPs of a call are
+ * 4 * D * H * B * pairs.  Returns < 0 (an rc_status) on an invalid layout. */
+int64_t rc_pairs(const rc_layout* L, int32_t entry);
+
+/* Token count of a row class (rc_rows_kind); < 0 on an invalid layout. */
+int64_t rc_rows(const rc_layout* L, int32_t which);
+
+/* Bytes of fp32 workspace rc_step_masked_attention needs for `splits`
+ * key splits (0 when splits <= 1): splits * B * H * N_live * (D + 2) * 4.
+ * splits = 0 resolves the automatic choice first.  0 on invalid input. */
+size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits);
+
+/* The split count rc_step_masked_attention uses when passed splits = 0. */
+int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D);
+
+/* Static-subgraph prefill (Sec. 3.3; App. C, Eq. cost-pre).
+ *   q_static, k_static, v_static  [B, N_static, H, D]: the ST and R tokens in
+ *                                 sequence order (RC_ROWS_STATIC rows).
+ *   o_static                      [B, N_static, H, D] out, every static row
+ *                                 (anchor rows included: later layers of the
+ *                                 prefill read them; the caller drops them).
+ *   lse_static                    [B, H, N_static] fp32 out, nullable.
+ *   k_cache, v_cache              [B, H, N_cached, D] out: bit copies of the
+ *                                 K/V rows of the cached segments (Eq. 2).
+ * Rows with no visible key get O = 0 and LSE = -inf. */
+rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                            const void* q_static, const void* k_static, const void* v_static,
+                            int64_t tok_stride, void* o_static, float* lse_static,
+                            void* k_cache, void* v_cache, void* stream);
+
+/* Per-denoising-step masked attention (App. C, Eq. cost-step).
+ *   q_live, k_live, v_live  [B, N_live, H, D]: LT and X tokens in sequence order.
+ *   k_cache, v_cache        [B, H, N_cached, D] as written by rc_ref_kv_prefill.
+ *   o_live                  [B, N_live, H, D] out;  lse_live [B, H, N_live] fp32, nullable.
+ *   splits                  key splits per query tile (split-KV); 0 = automatic,
+ *                           1 = none.  splits > 1 needs `workspace` (device,
+ *                           16-byte aligned) of rc_step_workspace_bytes bytes;
+ *                           partials are merged in a fixed order. */
+rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                   const void* q_live, const void* k_live, const void* v_live,
+                                   int64_t tok_stride, const void* k_cache, const void* v_cache,
+                                   void* o_live, float* lse_live, int32_t splits,
+                                   void* workspace, size_t ws_bytes, void* stream);
+
+/* Full-recompute baseline: every row of the sequence under L's mask.
+ *   q, k, v [B, N, H, D] with N = all tokens;  o [B, N, H, D];  lse [B, H, N] nullable. */
+rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                            const void* q, const void* k, const void* v, int64_t tok_stride,
+                            void* o, float* lse, void* stream);
+
+/* Static description of a status code. */
+const char* rc_status_string(rc_status s);
+
+/* Message for the last error on the calling thread ("" if none). */
+const char* rc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REFCACHE_H */

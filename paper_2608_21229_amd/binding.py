@@ -1,0 +1,241 @@
+"""ctypes binding of librefcache (include/refcache.h).
+
+Argument marshalling only: tensors are passed as device pointers and the
+current torch stream as a hipStream_t; every step of the computation runs in
+the library's HIP kernels.  torch supplies device memory and streams.
+
+Loading fails loudly if the library has not been built
+(``python -m paper_2608_21229_amd.build``): there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Iterable, Optional, Sequence, Tuple
+
+RC_MAX_SEGMENTS = 32
+RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP = 0, -1, -2, -3, -4, -5
+SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
+MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE = 0, 1, 2, 3
+ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL = 0, 1, 2
+ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL = 0, 1, 2, 3
+MASKS = {"paper": MASK_PAPER, "perref": MASK_PERREF, "isolated": MASK_ISOLATED, "dense": MASK_DENSE}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librefcache.so")
+
+
+class RcError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"librefcache status {status}: {message}")
+        self.status = status
+
+
+class _Segment(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("len", ctypes.c_int32)]
+
+
+class rc_layout(ctypes.Structure):
+    _fields_ = [("n_seg", ctypes.c_int32),
+                ("seg", _Segment * RC_MAX_SEGMENTS),
+                ("visible", ctypes.c_uint32 * RC_MAX_SEGMENTS)]
+
+
+_LIB = None
+_vp, _i32, _i64, _f32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+_PL = ctypes.POINTER(rc_layout)
+SIGNATURES = {
+    "rc_layout_preset": (_i32, [_PL, _i32]),
+    "rc_layout_validate": (_i32, [_PL, _i32]),
+    "rc_pairs": (_i64, [_PL, _i32]),
+    "rc_rows": (_i64, [_PL, _i32]),
+    "rc_step_workspace_bytes": (_sz, [_PL, _i32, _i32, _i32, _i32]),
+    "rc_step_auto_splits": (_i32, [_PL, _i32, _i32, _i32]),
+    "rc_ref_kv_prefill": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp]),
+    "rc_step_masked_attention": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
+                                        _i32, _vp, _sz, _vp]),
+    "rc_full_attention": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "rc_status_string": (ctypes.c_char_p, [_i32]),
+    "rc_last_error": (ctypes.c_char_p, []),
+}
+
+
+def lib():
+    """The loaded library; raises if it was not built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_21229_amd.build` "
+                               "(there is no CPU fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int):
+    if status != RC_OK:
+        raise RcError(status, lib().rc_last_error().decode())
+
+
+class Layout:
+    """Segment table + block mask (rc_layout).
+
+    segments: (kind, length) pairs in sequence order, kinds SEG_*.
+    mask: a preset name ('paper', 'perref', 'isolated', 'dense'), a MASK_*
+    id, or an explicit query-first boolean matrix over segments.
+    """
+
+    def __init__(self, segments: Sequence[Tuple[int, int]], mask="perref"):
+        if not 1 <= len(segments) <= RC_MAX_SEGMENTS:
+            raise ValueError(f"need 1..{RC_MAX_SEGMENTS} segments")
+        self.c = rc_layout()
+        self.c.n_seg = len(segments)
+        for i, (k, n) in enumerate(segments):
+            self.c.seg[i].kind = int(k)
+            self.c.seg[i].len = int(n)
+        self.segments = [(int(k), int(n)) for k, n in segments]
+        if isinstance(mask, str) or isinstance(mask, int):
+            preset = MASKS[mask] if isinstance(mask, str) else mask
+            _check(lib().rc_layout_preset(ctypes.byref(self.c), preset))
+        else:
+            for q, row in enumerate(mask):
+                self.c.visible[q] = sum(1 << k for k, v in enumerate(row) if v)
+
+    @property
+    def visible(self):
+        n = self.c.n_seg
+        return [[bool(self.c.visible[q] >> k & 1) for k in range(n)] for q in range(n)]
+
+    def validate(self, entry: int) -> int:
+        return lib().rc_layout_validate(ctypes.byref(self.c), entry)
+
+    def pairs(self, entry: int) -> int:
+        v = lib().rc_pairs(ctypes.byref(self.c), entry)
+        if v < 0:
+            _check(int(v))
+        return int(v)
+
+    def rows(self, which: int) -> int:
+        v = lib().rc_rows(ctypes.byref(self.c), which)
+        if v < 0:
+            _check(int(v))
+        return int(v)
+
+    def workspace_bytes(self, B: int, H: int, D: int, splits: int = 0) -> int:
+        return int(lib().rc_step_workspace_bytes(ctypes.byref(self.c), B, H, D, splits))
+
+    def auto_splits(self, B: int, H: int, D: int) -> int:
+        return int(lib().rc_step_auto_splits(ctypes.byref(self.c), B, H, D))
+
+
+# ---------------------------------------------------------------- tensor entry points
+def _torch():
+    import torch
+    return torch
+
+
+def _tok_stride(*ts) -> int:
+    strides = set()
+    for t in ts:
+        B, N, H, D = t.shape
+        if t.stride(3) != 1 or t.stride(2) != D or (B > 1 and t.stride(0) != N * t.stride(1)):
+            raise ValueError("Q/K/V must be [B, N, H, D] with D contiguous, head stride D and batch stride N*tok_stride")
+        strides.add(t.stride(1))
+    if len(strides) != 1:
+        raise ValueError("Q, K and V must share one token stride")
+    return strides.pop()
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _expect(t, shape, dtype_name, what):
+    """Outputs and the cache use the library's contiguous layouts."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous() or str(t.dtype) != dtype_name:
+        raise ValueError(f"{what} must be a contiguous {dtype_name} tensor of shape {tuple(shape)}, "
+                         f"got {str(t.dtype)} {tuple(t.shape)} contiguous={t.is_contiguous()}")
+
+
+def _stream(stream) -> Optional[int]:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_cache=None,
+                   scale: Optional[float] = None, want_lse: bool = False, stream=None):
+    """Static-subgraph prefill.  q/k/v: [B, N_static, H, D] bf16 (ST and R
+    tokens in sequence order).  Returns (o, lse or None, k_cache, v_cache)."""
+    torch = _torch()
+    B, N, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    ts = _tok_stride(q, k, v)
+    nc = layout.rows(ROWS_CACHED)
+    if o is None:
+        o = torch.empty((B, N, H, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    if k_cache is None:
+        k_cache = torch.empty((B, H, nc, D), dtype=torch.bfloat16, device=q.device)
+    if v_cache is None:
+        v_cache = torch.empty((B, H, nc, D), dtype=torch.bfloat16, device=q.device)
+    _expect(o, (B, N, H, D), "torch.bfloat16", "o")
+    _expect(lse, (B, H, N), "torch.float32", "lse")
+    _expect(k_cache, (B, H, nc, D), "torch.bfloat16", "k_cache")
+    _expect(v_cache, (B, H, nc, D), "torch.bfloat16", "v_cache")
+    _check(lib().rc_ref_kv_prefill(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                   v.data_ptr(), ts, o.data_ptr(), _ptr(lse), k_cache.data_ptr(),
+                                   v_cache.data_ptr(), _stream(stream)))
+    return o, lse, k_cache, v_cache
+
+
+def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse=None, splits: int = 0,
+                          workspace=None, scale: Optional[float] = None, want_lse: bool = False, stream=None):
+    """Per-step attention.  q/k/v: [B, N_live, H, D] bf16 (LT and X tokens);
+    k_cache/v_cache: [B, H, N_cached, D].  Returns (o, lse or None)."""
+    torch = _torch()
+    B, N, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    ts = _tok_stride(q, k, v)
+    if o is None:
+        o = torch.empty((B, N, H, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    nc = layout.rows(ROWS_CACHED)
+    _expect(o, (B, N, H, D), "torch.bfloat16", "o")
+    _expect(lse, (B, H, N), "torch.float32", "lse")
+    _expect(k_cache, (B, H, nc, D), "torch.bfloat16", "k_cache")
+    _expect(v_cache, (B, H, nc, D), "torch.bfloat16", "v_cache")
+    need = layout.workspace_bytes(B, H, D, splits)
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check(lib().rc_step_masked_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                          v.data_ptr(), ts, _ptr(k_cache), _ptr(v_cache), o.data_ptr(),
+                                          _ptr(lse), splits, _ptr(workspace) if need else None,
+                                          need, _stream(stream)))
+    return o, lse
+
+
+def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[float] = None,
+                   want_lse: bool = False, stream=None):
+    """Full recompute over all rows.  q/k/v: [B, N, H, D] bf16.  Returns (o, lse or None)."""
+    torch = _torch()
+    B, N, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    ts = _tok_stride(q, k, v)
+    if o is None:
+        o = torch.empty((B, N, H, D), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _expect(o, (B, N, H, D), "torch.bfloat16", "o")
+    _expect(lse, (B, H, N), "torch.float32", "lse")
+    _check(lib().rc_full_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                   v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _stream(stream)))
+    return o, lse

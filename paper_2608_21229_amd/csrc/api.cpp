@@ -1,0 +1,287 @@
+// extern "C" entry points of librefcache: argument validation, planning and
+// kernel launches.  Every check runs before the first HIP call, so a failing
+// call launches nothing and needs no GPU.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "rc_internal.h"
+
+namespace rc {
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+rc_status check_dims(int32_t B, int32_t H, int32_t D, float scale) {
+  if (B < 1 || H < 1 || B > 65535 || H > 65535) {
+    set_error("B = %d, H = %d: each must be in [1, 65535]", B, H);
+    return RC_ERR_ARG;
+  }
+  if (D != 64 && D != 128) {
+    set_error("head_dim %d is not supported (64 or 128)", D);
+    return RC_ERR_UNSUPPORTED;
+  }
+  if (!(scale > 0.f) || !isfinite(scale)) {
+    set_error("softmax scale must be finite and > 0 (got %g)", (double)scale);
+    return RC_ERR_ARG;
+  }
+  return RC_OK;
+}
+
+rc_status check_ptr(const void* p, const char* name) {
+  if (!p) {
+    set_error("%s is null", name);
+    return RC_ERR_ARG;
+  }
+  if (!aligned16(p)) {
+    set_error("%s is not 16-byte aligned", name);
+    return RC_ERR_ARG;
+  }
+  return RC_OK;
+}
+
+rc_status check_lse(const float* p, const char* name) {
+  if (p && (reinterpret_cast<uintptr_t>(p) & 3u)) {
+    set_error("%s is not 4-byte aligned", name);
+    return RC_ERR_ARG;
+  }
+  return RC_OK;
+}
+
+rc_status check_stride(int64_t tok_stride, int32_t H, int32_t D) {
+  if (tok_stride < int64_t(H) * D || (tok_stride & 7)) {
+    set_error("tok_stride %lld must be >= H*D = %d and a multiple of 8", (long long)tok_stride, H * D);
+    return RC_ERR_ARG;
+  }
+  if (tok_stride > (int64_t(1) << 32)) {
+    set_error("tok_stride %lld is too large", (long long)tok_stride);
+    return RC_ERR_ARG;
+  }
+  return RC_OK;
+}
+
+rc_status check_grid(const Params& p) {
+  const int64_t blocks = int64_t(p.B) * p.H * p.n_qtiles * p.splits;
+  if (blocks >= (int64_t(1) << 31)) {
+    set_error("launch of %lld work-groups exceeds the grid limit", (long long)blocks);
+    return RC_ERR_ARG;
+  }
+  return RC_OK;
+}
+
+#define RC_TRY(x)                  \
+  do {                             \
+    rc_status _s = (x);            \
+    if (_s != RC_OK) return _s;    \
+  } while (0)
+
+rc_status hip_status(int err, const char* what) {
+  if (err != 0) {
+    set_error("%s: HIP error %d", what, err);
+    return RC_ERR_HIP;
+  }
+  return RC_OK;
+}
+
+void fill_common(Params& p, int32_t B, int32_t H, float scale) {
+  p.B = B;
+  p.H = H;
+  p.splits = 1;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  p.lse = nullptr;
+  p.ws_o = nullptr;
+  p.ws_ml = nullptr;
+  p.src[1] = KeySrc{nullptr, nullptr, 0, 0, 0};
+}
+
+}  // namespace
+}  // namespace rc
+
+using namespace rc;
+
+extern "C" {
+
+rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                            const void* q_static, const void* k_static, const void* v_static,
+                            int64_t tok_stride, void* o_static, float* lse_static, void* k_cache,
+                            void* v_cache, void* stream) {
+  RC_TRY(check_layout(L, RC_ENTRY_PREFILL));
+  RC_TRY(check_dims(B, H, D, scale));
+  RC_TRY(check_stride(tok_stride, H, D));
+  const int64_t n_static = count_rows(L, RowSet::Static);
+  const int64_t n_cached = count_cached_rows(L);
+  if (n_static == 0) return RC_OK;  // no ST/R segment: nothing to prefill
+  RC_TRY(check_ptr(q_static, "q_static"));
+  RC_TRY(check_ptr(k_static, "k_static"));
+  RC_TRY(check_ptr(v_static, "v_static"));
+  RC_TRY(check_ptr(o_static, "o_static"));
+  RC_TRY(check_lse(lse_static, "lse_static"));
+  if (n_cached > 0) {
+    RC_TRY(check_ptr(k_cache, "k_cache"));
+    RC_TRY(check_ptr(v_cache, "v_cache"));
+  }
+  Params p;
+  memset(&p, 0, sizeof p);
+  fill_common(p, B, H, scale);
+  RC_TRY(plan(L, RC_ENTRY_PREFILL, p));
+  RC_TRY(check_grid(p));
+  p.q = static_cast<const uint16_t*>(q_static);
+  p.q_st = tok_stride;
+  p.q_sb = tok_stride * n_static;
+  p.o = static_cast<uint16_t*>(o_static);
+  p.o_st = int64_t(H) * D;
+  p.o_sb = p.o_st * n_static;
+  p.lse = lse_static;
+  p.src[0] = KeySrc{static_cast<const uint16_t*>(k_static), static_cast<const uint16_t*>(v_static),
+                    tok_stride * n_static, D, tok_stride};
+
+  CacheStoreParams c;
+  memset(&c, 0, sizeof c);
+  if (n_cached > 0) {
+    c.k_src = static_cast<const uint16_t*>(k_static);
+    c.v_src = static_cast<const uint16_t*>(v_static);
+    c.k_dst = static_cast<uint16_t*>(k_cache);
+    c.v_dst = static_cast<uint16_t*>(v_cache);
+    c.src_st = tok_stride;
+    c.src_sb = tok_stride * n_static;
+    c.B = B;
+    c.H = H;
+    c.D = D;
+    c.n_cached = int32_t(n_cached);
+    const uint32_t cm = cached_mask(L);
+    int32_t srow = 0, drow = 0;
+    for (int i = 0; i < L->n_seg; ++i) {
+      if (!is_static_kind(L->seg[i].kind)) continue;
+      if (cm >> i & 1u) {
+        c.seg[c.n_copy++] = CopySeg{srow, L->seg[i].len, drow};
+        drow += L->seg[i].len;
+      }
+      srow += L->seg[i].len;
+    }
+    c.total_rows = drow;
+  }
+  RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
+  if (n_cached > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
+  return RC_OK;
+}
+
+int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D) {
+  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 1;
+  if (B < 1 || H < 1 || (D != 64 && D != 128)) return 1;
+  Params p;
+  memset(&p, 0, sizeof p);
+  p.B = B;
+  p.H = H;
+  if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
+  return auto_splits(p);
+}
+
+size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
+  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
+  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < 0) return 0;
+  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
+  if (splits <= 1) return 0;
+  const int64_t n_live = count_rows(L, RowSet::Live);
+  return size_t(splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
+}
+
+rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                   const void* q_live, const void* k_live, const void* v_live,
+                                   int64_t tok_stride, const void* k_cache, const void* v_cache,
+                                   void* o_live, float* lse_live, int32_t splits, void* workspace,
+                                   size_t ws_bytes, void* stream) {
+  RC_TRY(check_layout(L, RC_ENTRY_STEP));
+  RC_TRY(check_dims(B, H, D, scale));
+  RC_TRY(check_stride(tok_stride, H, D));
+  if (splits < 0 || splits > kMaxSplits) {
+    set_error("splits = %d must be in [0, %d]", splits, kMaxSplits);
+    return RC_ERR_ARG;
+  }
+  const int64_t n_live = count_rows(L, RowSet::Live);
+  const int64_t n_cached = count_cached_rows(L);
+  if (n_live == 0) return RC_OK;  // no LT/X segment: nothing to attend
+  RC_TRY(check_ptr(q_live, "q_live"));
+  RC_TRY(check_ptr(k_live, "k_live"));
+  RC_TRY(check_ptr(v_live, "v_live"));
+  RC_TRY(check_ptr(o_live, "o_live"));
+  RC_TRY(check_lse(lse_live, "lse_live"));
+  if (n_cached > 0) {
+    RC_TRY(check_ptr(k_cache, "k_cache"));
+    RC_TRY(check_ptr(v_cache, "v_cache"));
+  }
+  Params p;
+  memset(&p, 0, sizeof p);
+  fill_common(p, B, H, scale);
+  RC_TRY(plan(L, RC_ENTRY_STEP, p));
+  p.splits = splits == 0 ? auto_splits(p) : splits;
+  RC_TRY(check_grid(p));
+  p.q = static_cast<const uint16_t*>(q_live);
+  p.q_st = tok_stride;
+  p.q_sb = tok_stride * n_live;
+  p.o = static_cast<uint16_t*>(o_live);
+  p.o_st = int64_t(H) * D;
+  p.o_sb = p.o_st * n_live;
+  p.lse = lse_live;
+  p.src[0] = KeySrc{static_cast<const uint16_t*>(k_live), static_cast<const uint16_t*>(v_live),
+                    tok_stride * n_live, D, tok_stride};
+  p.src[1] = KeySrc{static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache),
+                    int64_t(H) * n_cached * D, n_cached * D, D};
+  CombineParams c;
+  memset(&c, 0, sizeof c);
+  if (p.splits > 1) {
+    const size_t need = size_t(p.splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
+    if (!workspace || !aligned16(workspace) || ws_bytes < need) {
+      set_error("split-KV with %d splits needs a 16-byte aligned workspace of %zu bytes (got %zu)", p.splits,
+                need, workspace ? ws_bytes : size_t(0));
+      return RC_ERR_WORKSPACE;
+    }
+    p.ws_o = static_cast<float*>(workspace);
+    p.ws_ml = p.ws_o + size_t(p.splits) * B * H * n_live * D;
+    c.ws_o = p.ws_o;
+    c.ws_ml = p.ws_ml;
+    c.o = p.o;
+    c.lse = lse_live;
+    c.o_sb = p.o_sb;
+    c.o_st = p.o_st;
+    c.B = B;
+    c.H = H;
+    c.D = D;
+    c.n_rows = int32_t(n_live);
+    c.splits = p.splits;
+  }
+  RC_TRY(hip_status(launch_attention(p, D, stream), "step attention launch"));
+  if (p.splits > 1) RC_TRY(hip_status(launch_combine(c, stream), "split-KV combine launch"));
+  return RC_OK;
+}
+
+rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q,
+                            const void* k, const void* v, int64_t tok_stride, void* o, float* lse,
+                            void* stream) {
+  RC_TRY(check_layout(L, RC_ENTRY_FULL));
+  RC_TRY(check_dims(B, H, D, scale));
+  RC_TRY(check_stride(tok_stride, H, D));
+  RC_TRY(check_ptr(q, "q"));
+  RC_TRY(check_ptr(k, "k"));
+  RC_TRY(check_ptr(v, "v"));
+  RC_TRY(check_ptr(o, "o"));
+  RC_TRY(check_lse(lse, "lse"));
+  const int64_t n = count_rows(L, RowSet::All);
+  Params p;
+  memset(&p, 0, sizeof p);
+  fill_common(p, B, H, scale);
+  RC_TRY(plan(L, RC_ENTRY_FULL, p));
+  RC_TRY(check_grid(p));
+  p.q = static_cast<const uint16_t*>(q);
+  p.q_st = tok_stride;
+  p.q_sb = tok_stride * n;
+  p.o = static_cast<uint16_t*>(o);
+  p.o_st = int64_t(H) * D;
+  p.o_sb = p.o_st * n;
+  p.lse = lse;
+  p.src[0] = KeySrc{static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), tok_stride * n, D,
+                    tok_stride};
+  RC_TRY(hip_status(launch_attention(p, D, stream), "full attention launch"));
+  return RC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,410 @@
+// Block-masked flash attention forward for gfx950 (CDNA4), plus the split-KV
+// combine and the reference K/V cache store.
+//
+// Method: softmax(scale * Q K^T) V over the visible key segments of each
+// query segment (Sec. 3.3 mask; App. C interaction counts).  The planner
+// hands every work-group a BM = 128-row query tile inside one segment and the
+// list of visible key ranges; invisible segments are never loaded.
+//
+// Work-group = 4 waves of 64 lanes, each wave owns 32 query rows.  Per 64-key
+// tile:
+//   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = the
+//                   wave's Q rows held in registers for the whole kernel.
+//                   The 32x32 accumulator puts one query per lane (lane % 32)
+//                   and 16 keys per lane, so the row max needs only in-lane
+//                   max plus one exchange between the two 32-lane halves.
+//   online softmax  exp2 with scale*log2(e) folded into one FMA; the running
+//                   max is refreshed lazily (only when a row's max grows by
+//                   more than 2^8), which is exact because the same stale max
+//                   scales both the sum and the accumulator.
+//   O^T += V^T P^T  A = V^T read from row-major V in LDS with the gfx950
+//                   transpose read ds_read_b64_tr_b16, B = P^T straight from
+//                   the S^T accumulator registers (bf16), so the output also
+//                   has one query per lane and the softmax statistics never
+//                   leave their lane.
+// K/V tiles are double-buffered in LDS with 16-byte global loads (coalesced:
+// 16 lanes cover one 256-byte row) and an XOR swizzle at 16-byte granularity
+// that keeps both the 128-bit K reads and the transpose V reads free of bank
+// conflicts.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rc_internal.h"
+
+namespace rc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int kThreads = 256;
+constexpr float kLazyThreshold = 8.0f;  // log2 units: rescale when a row max grows by > 2^8
+
+__device__ __forceinline__ int swz(int row, int g, int gr) {
+  return g ^ ((((row & 7) << 1) | ((row >> 3) & 1)) & (gr - 1));
+}
+
+__device__ __forceinline__ float max_halves(float x) {
+  // max of this lane and lane ^ 32 (the two halves hold different keys of the same query)
+  auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
+}
+
+__device__ __forceinline__ float sum_halves(float x) {
+  auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+}
+
+// Cursor over the key tiles of one query segment: (range, tile inside range).
+struct Cursor {
+  int r, t;
+};
+
+__device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int kt) {
+  Cursor c{qs.r0, kt};
+  for (int i = 0; i < qs.nr; ++i) {
+    const int n = p.range[qs.r0 + i].ntiles;
+    if (c.t < n) break;
+    c.t -= n;
+    ++c.r;
+  }
+  return c;
+}
+
+__device__ __forceinline__ void cursor_next(const Params& p, Cursor& c) {
+  if (++c.t >= p.range[c.r].ntiles) {
+    c.t = 0;
+    ++c.r;
+  }
+}
+
+template <int D>
+struct TileRegs {
+  static constexpr int kLoads = kBN * (D / 8) / kThreads;  // 16-byte granules per thread
+  u32x4 k[kLoads];
+  u32x4 v[kLoads];
+};
+
+template <int D>
+__device__ __forceinline__ void load_tile(const Params& p, const Cursor& c, int b, int h, int tid,
+                                          TileRegs<D>& regs, int& valid) {
+  constexpr int GR = D / 8;
+  const KeyRange& rg = p.range[c.r];
+  const KeySrc& s = p.src[rg.src];
+  const int key0 = rg.start + c.t * kBN;
+  valid = min(kBN, rg.len - c.t * kBN);
+  const int64_t base = int64_t(b) * s.sb + int64_t(h) * s.sh + int64_t(key0) * s.st;
+#pragma unroll
+  for (int i = 0; i < TileRegs<D>::kLoads; ++i) {
+    const int gi = tid + kThreads * i;
+    const int row = gi / GR, g = gi % GR;
+    if (row < valid) {
+      const int64_t off = base + int64_t(row) * s.st + g * 8;
+      regs.k[i] = *reinterpret_cast<const u32x4*>(s.k + off);
+      regs.v[i] = *reinterpret_cast<const u32x4*>(s.v + off);
+    } else {
+      regs.k[i] = u32x4{0u, 0u, 0u, 0u};
+      regs.v[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_tile(uint16_t* ks, uint16_t* vs, int tid, const TileRegs<D>& regs) {
+  constexpr int GR = D / 8;
+#pragma unroll
+  for (int i = 0; i < TileRegs<D>::kLoads; ++i) {
+    const int gi = tid + kThreads * i;
+    const int row = gi / GR, g = gi % GR;
+    const int off = row * D + swz(row, g, GR) * 8;
+    *reinterpret_cast<u32x4*>(ks + off) = regs.k[i];
+    *reinterpret_cast<u32x4*>(vs + off) = regs.v[i];
+  }
+}
+
+template <int D, bool kSplit>
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
+  constexpr int GR = D / 8;
+  constexpr int NDC = D / 16;  // 16-wide d chunks of the QK^T contraction
+  constexpr int NB = D / 32;   // 32-wide d blocks of the output
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2][2][kBN * D];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hh = lane >> 5;  // which 32-lane half
+
+  // ---- work item: XCD-aware remap so consecutive logical items (same head)
+  // share one XCD's L2.  The hardware deals blocks to the 8 XCDs round-robin.
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, kx = bid >> 3, per = nblk >> 3, rem = nblk & 7;
+  const int w = (xcd < rem) ? xcd * (per + 1) + kx : rem * (per + 1) + (xcd - rem) * per + kx;
+  const int split = w % p.splits;
+  int rest = w / p.splits;
+  const int t = rest % p.n_qtiles;
+  rest /= p.n_qtiles;
+  const int h = rest % p.H, b = rest / p.H;
+
+  int qi = 0;
+  while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
+  const QSeg qs = p.qseg[qi];
+  const int seg_row0 = (t - qs.tile0) * kBM;
+  const int rows_valid = min(kBM, qs.len - seg_row0);
+  const int row0 = qs.row0 + seg_row0;  // first row of the tile in the Q/O buffers
+  const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
+  const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+
+  // ---- Q fragment (B operand of S^T = K Q^T): lane holds query (lane % 32),
+  // d = 16*dc + 8*hh .. +7.
+  const int my_row = wave * 32 + (lane & 31);
+  const bool row_ok = my_row < rows_valid;
+  bf16x8 qf[NDC];
+  {
+    const uint16_t* qp = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row) * p.q_st + int64_t(h) * D + hh * 8;
+#pragma unroll
+    for (int dc = 0; dc < NDC; ++dc) {
+      u32x4 raw = row_ok ? *reinterpret_cast<const u32x4*>(qp + dc * 16) : u32x4{0u, 0u, 0u, 0u};
+      qf[dc] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+
+  f32x16 oacc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[nb][r] = 0.f;
+  float m_used = -INFINITY;  // running max in log2 units
+  float lsum = 0.f;          // this half's partial row sum
+  const float c = p.scale_log2;
+
+  TileRegs<D> regs;
+  Cursor cur = cursor_at(p, qs, kt_begin);
+  int valid_cur = 0, valid_next = 0;
+  if (kt_begin < kt_end) {
+    load_tile<D>(p, cur, b, h, tid, regs, valid_cur);
+    store_tile<D>(smem[0][0], smem[0][1], tid, regs);
+  }
+  __syncthreads();
+
+  for (int kt = kt_begin; kt < kt_end; ++kt) {
+    const int stage = (kt - kt_begin) & 1;
+    const bool more = kt + 1 < kt_end;
+    Cursor nxt = cur;
+    if (more) {
+      cursor_next(p, nxt);
+      load_tile<D>(p, nxt, b, h, tid, regs, valid_next);
+    }
+    const uint16_t* ks = smem[stage][0];
+    const uint16_t* vs = smem[stage][1];
+
+    // ---- S^T = K Q^T for 64 keys: two 32-key blocks
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+      const int krow = kb * 32 + (lane & 31);
+#pragma unroll
+      for (int dc = 0; dc < NDC; ++dc) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + hh, GR) * 8);
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[dc], sacc[kb], 0, 0, 0);
+      }
+    }
+    // ragged tail: keys past the end of the range score -inf
+    if (valid_cur < kBN) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          if (key >= valid_cur) sacc[kb][r] = -INFINITY;
+        }
+    }
+    // ---- online softmax (row = this lane's query)
+    float mx = sacc[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+    const float mt = max_halves(mx) * c;
+    if (__any(mt > m_used + kLazyThreshold)) {
+      const float m_new = fmaxf(m_used, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
+      lsum *= alpha;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
+      m_used = m_new;
+    }
+    bf16x8 pf[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
+        lsum += e;
+        pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
+      }
+    // ---- O^T += V^T P^T: 16 keys per MFMA, 32 d-rows per MFMA
+    {
+      const int grp = lane >> 4, li = lane & 15;
+      const int dhalf = grp & 1;
+      const int rsub = li >> 2, dsub = 4 * (li & 3);
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int d = nb * 32 + dhalf * 16 + dsub;
+          const int r0 = cc * 16 + 4 * hh + rsub;
+          const int r1 = r0 + 8;
+          const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
+          const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
+          typedef short i16x8 __attribute__((ext_vector_type(8)));
+          const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pf[cc], oacc[nb], 0, 0, 0);
+        }
+      }
+    }
+    if (more) store_tile<D>(smem[stage ^ 1][0], smem[stage ^ 1][1], tid, regs);
+    __syncthreads();
+    cur = nxt;
+    valid_cur = valid_next;
+  }
+
+  // ---- epilogue
+  const float l_tot = sum_halves(lsum);
+  if (!row_ok) return;
+  const int grow = row0 + my_row;
+  if constexpr (kSplit) {
+    const int64_t prow = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + grow;
+    float* op = p.ws_o + prow * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = nb * 32 + 8 * q4 + 4 * hh;
+        float4 v4 = make_float4(oacc[nb][4 * q4], oacc[nb][4 * q4 + 1], oacc[nb][4 * q4 + 2], oacc[nb][4 * q4 + 3]);
+        *reinterpret_cast<float4*>(op + d) = v4;
+      }
+    if (hh == 0) {
+      p.ws_ml[prow * 2] = m_used;
+      p.ws_ml[prow * 2 + 1] = l_tot;
+    }
+  } else {
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(grow) * p.o_st + int64_t(h) * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = nb * 32 + 8 * q4 + 4 * hh;
+        __bf16 o4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(oacc[nb][4 * q4 + j] * inv);
+        *reinterpret_cast<u32x2*>(op + d) = __builtin_bit_cast(u32x2, o4);
+      }
+    if (p.lse && hh == 0)
+      p.lse[(int64_t(b) * p.H + h) * p.n_rows + grow] =
+          l_tot > 0.f ? m_used * 0.69314718055994531f + __logf(l_tot) : -INFINITY;
+  }
+}
+
+// Split-KV merge: O = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s, in split order.
+// One thread per (row, 4 consecutive d).
+__global__ __launch_bounds__(256) void combine_kernel(const CombineParams c) {
+  const int dq = c.D / 4;
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t total = int64_t(c.B) * c.H * c.n_rows * dq;
+  if (idx >= total) return;
+  const int d4 = int(idx % dq);
+  const int64_t bhr = idx / dq;  // (b*H + h)*n_rows + row
+  const int row = int(bhr % c.n_rows);
+  const int64_t bh = bhr / c.n_rows;
+  const int h = int(bh % c.H), b = int(bh / c.H);
+  const int64_t plane = int64_t(c.B) * c.H * c.n_rows;
+  float M = -INFINITY;
+  for (int s = 0; s < c.splits; ++s) {
+    const float ls = c.ws_ml[(s * plane + bhr) * 2 + 1];
+    if (ls > 0.f) M = fmaxf(M, c.ws_ml[(s * plane + bhr) * 2]);
+  }
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float l = 0.f;
+  if (M != -INFINITY) {
+    for (int s = 0; s < c.splits; ++s) {
+      const float ls = c.ws_ml[(s * plane + bhr) * 2 + 1];
+      if (!(ls > 0.f)) continue;
+      const float wgt = __builtin_amdgcn_exp2f(c.ws_ml[(s * plane + bhr) * 2] - M);
+      const float4 o = *reinterpret_cast<const float4*>(c.ws_o + (s * plane + bhr) * c.D + 4 * d4);
+      acc.x += wgt * o.x;
+      acc.y += wgt * o.y;
+      acc.z += wgt * o.z;
+      acc.w += wgt * o.w;
+      l += wgt * ls;
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  __bf16 o4[4] = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv), (__bf16)(acc.w * inv)};
+  uint16_t* op = c.o + int64_t(b) * c.o_sb + int64_t(row) * c.o_st + int64_t(h) * c.D + 4 * d4;
+  *reinterpret_cast<u32x2*>(op) = __builtin_bit_cast(u32x2, o4);
+  if (c.lse && d4 == 0)
+    c.lse[bhr] = l > 0.f ? M * 0.69314718055994531f + __logf(l) : -INFINITY;
+}
+
+// Cache store: one thread per 16-byte granule of one cached (b, h, row).
+__global__ __launch_bounds__(256) void cache_store_kernel(const CacheStoreParams c) {
+  const int gr = c.D / 8;
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t total = int64_t(c.B) * c.H * c.total_rows * gr;
+  if (idx >= total) return;
+  const int g = int(idx % gr);
+  int64_t rest = idx / gr;
+  const int drow = int(rest % c.total_rows);
+  rest /= c.total_rows;
+  const int h = int(rest % c.H), b = int(rest / c.H);
+  int si = 0;
+  while (si + 1 < c.n_copy && c.seg[si + 1].dst_row0 <= drow) ++si;
+  const int srow = c.seg[si].src_row0 + (drow - c.seg[si].dst_row0);
+  const int64_t so = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
+  const int64_t dof = ((int64_t(b) * c.H + h) * c.n_cached + drow) * c.D + g * 8;
+  *reinterpret_cast<u32x4*>(c.k_dst + dof) = *reinterpret_cast<const u32x4*>(c.k_src + so);
+  *reinterpret_cast<u32x4*>(c.v_dst + dof) = *reinterpret_cast<const u32x4*>(c.v_src + so);
+}
+
+}  // namespace
+
+int launch_attention(const Params& p, int D, void* stream) {
+  const int64_t blocks = int64_t(p.B) * p.H * p.n_qtiles * p.splits;
+  if (blocks == 0) return 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool split = p.splits > 1;
+  if (D == 128) {
+    if (split) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), dim3(blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, s, p);
+  } else {
+    if (split) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, p);
+  }
+  return int(hipGetLastError());
+}
+
+int launch_combine(const CombineParams& c, void* stream) {
+  const int64_t total = int64_t(c.B) * c.H * c.n_rows * (c.D / 4);
+  if (total == 0) return 0;
+  hipLaunchKernelGGL(combine_kernel, dim3((total + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream), c);
+  return int(hipGetLastError());
+}
+
+int launch_cache_store(const CacheStoreParams& c, void* stream) {
+  const int64_t total = int64_t(c.B) * c.H * c.total_rows * (c.D / 8);
+  if (total == 0) return 0;
+  hipLaunchKernelGGL(cache_store_kernel, dim3((total + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream), c);
+  return int(hipGetLastError());
+}
+
+}  // namespace rc

@@ -1,0 +1,104 @@
+// Internal schedule shared by the host planner (layout.cpp, api.cpp) and the
+// HIP kernels (attn_fwd.hip).  Not part of the public ABI.
+//
+// The planner turns an rc_layout plus an entry point into:
+//   * query segments: which rows of the Q/O buffers one segment occupies and
+//     how many BM-row tiles it splits into (a tile never straddles segments);
+//   * key ranges: for each query segment, the visible key segments merged into
+//     contiguous runs inside one key source, in sequence order.  Invisible
+//     segments never appear, so masked blocks cost no loads and no MFMA.
+// Two key sources exist: source 0 is the entry's own K/V buffer ([B,N,H,D]),
+// source 1 is the reference K/V cache ([B,H,N_cached,D]).
+#pragma once
+#include <stdint.h>
+
+#include "refcache.h"
+
+namespace rc {
+
+constexpr int kBM = 128;          // query rows per work-group (4 waves x 32)
+constexpr int kBN = 64;           // keys per K/V tile
+constexpr int kMaxRanges = 96;    // merged key ranges over all query segments
+constexpr int kMaxSplits = 32;
+
+struct KeyRange {
+  int32_t start;   // first key token inside its source
+  int32_t len;     // tokens
+  int32_t src;     // 0 = entry buffer, 1 = cache
+  int32_t ntiles;  // ceil(len / kBN)
+};
+
+struct QSeg {
+  int32_t row0;    // first row inside the Q/O buffers
+  int32_t len;     // rows
+  int32_t tile0;   // index of this segment's first query tile
+  int32_t r0;      // first key range
+  int32_t nr;      // number of key ranges
+  int32_t ktiles;  // key tiles over all its ranges
+};
+
+struct KeySrc {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t sb, sh, st;  // element strides: batch, head, token
+};
+
+struct Params {
+  const uint16_t* q;
+  int64_t q_sb, q_st;  // element strides of Q: batch, token (head stride = D)
+  uint16_t* o;
+  int64_t o_sb, o_st;
+  float* lse;          // [B, H, n_rows] or null
+  float* ws_o;         // split partials [splits, B, H, n_rows, D] (unnormalised)
+  float* ws_ml;        // split partials [splits, B, H, n_rows, 2] (max in log2 units, sum)
+  KeySrc src[2];
+  int32_t B, H, n_rows, n_qseg, n_qtiles, splits;
+  float scale_log2;    // softmax scale * log2(e)
+  QSeg qseg[RC_MAX_SEGMENTS];
+  KeyRange range[kMaxRanges];
+};
+
+// Cache store: copy rows of the cached segments from the static K/V buffers
+// ([B, N_static, H, D], token stride) into the cache ([B, H, N_cached, D]).
+struct CopySeg {
+  int32_t src_row0, len, dst_row0;
+};
+struct CacheStoreParams {
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  uint16_t* k_dst;
+  uint16_t* v_dst;
+  int64_t src_sb, src_st;
+  int32_t B, H, D, n_cached, n_copy, total_rows;
+  CopySeg seg[RC_MAX_SEGMENTS];
+};
+
+struct CombineParams {
+  const float* ws_o;
+  const float* ws_ml;
+  uint16_t* o;
+  float* lse;
+  int64_t o_sb, o_st;
+  int32_t B, H, D, n_rows, splits;
+};
+
+// Host-side planning (layout.cpp).
+enum class RowSet { Static, Live, All };
+bool is_static_kind(int32_t kind);
+bool is_live_kind(int32_t kind);
+rc_status check_layout(const rc_layout* L, int32_t entry);  // sets the thread error on failure
+uint32_t cached_mask(const rc_layout* L);                  // bit i: segment i is cached
+int64_t count_rows(const rc_layout* L, RowSet set);
+int64_t count_cached_rows(const rc_layout* L);
+// Fill p.qseg / p.range / n_qseg / n_qtiles / n_rows for an entry.
+rc_status plan(const rc_layout* L, int32_t entry, Params& p);
+int32_t auto_splits(const Params& p);
+
+void set_error(const char* fmt, ...);
+
+// Kernel launchers (attn_fwd.hip).  Return a hipError_t as int.
+int launch_attention(const Params& p, int D, void* stream);
+int launch_combine(const CombineParams& c, void* stream);
+int launch_cache_store(const CacheStoreParams& c, void* stream);
+
+}  // namespace rc

@@ -1,0 +1,194 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+include/refcache.h declares, computes presets / pair counts / row counts that
+agree with the oracle's independent statement, and rejects bad arguments with
+the documented status before any HIP call (so no GPU is needed)."""
+import ctypes
+import os
+import random
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_21229_amd as rc
+from paper_2608_21229_amd import binding
+from oracle import cost as oc
+from oracle import masks as om
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "refcache.h")
+FAKE = 0x7f0000000000   # 16-byte aligned, never dereferenced: every call below fails validation first
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(rc_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert len(names) >= 10
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\sT\s(rc_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    assert set(names) == set(binding.SIGNATURES), "binding signatures out of sync with the header"
+    L = rc.lib()
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def random_layout(rng):
+    n = rng.randint(1, 10)
+    kinds = [rng.choice([0, 1, 2, 3]) for _ in range(n)]
+    lens = [rng.choice([1, 2, 7, 64, 65, 100, 4096]) for _ in range(n)]
+    return kinds, lens
+
+
+@pytest.mark.parametrize("preset", ["paper", "perref", "isolated", "dense"])
+def test_presets_and_counts_match_oracle(preset):
+    rng = random.Random(7)
+    for _ in range(200):
+        kinds, lens = random_layout(rng)
+        L = rc.Layout(list(zip(kinds, lens)), preset)
+        vis = om.PRESETS[preset](kinds)
+        assert L.visible == vis
+        assert L.pairs(rc.ENTRY_FULL) == oc.visible_pairs(kinds, lens, vis, "all")
+        cacheable = om.is_cacheable(kinds, vis)
+        for entry, rows in ((rc.ENTRY_PREFILL, "static"), (rc.ENTRY_STEP, "live")):
+            if cacheable:
+                assert L.pairs(entry) == oc.visible_pairs(kinds, lens, vis, rows)
+            else:
+                assert L.validate(entry) == rc.RC_ERR_MASK_NOT_CACHEABLE
+        assert L.rows(rc.ROWS_STATIC) == sum(n for k, n in zip(kinds, lens) if k in (0, 3))
+        assert L.rows(rc.ROWS_LIVE) == sum(n for k, n in zip(kinds, lens) if k in (1, 2))
+        assert L.rows(rc.ROWS_ALL) == sum(lens)
+        assert L.rows(rc.ROWS_CACHED) == sum(lens[i] for i in om.cached_segments(kinds, vis))
+
+
+def test_headline_counts():
+    segs = [(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5
+    L = rc.Layout(segs, "perref")
+    assert L.pairs(rc.ENTRY_STEP) == 115_900_416
+    assert L.pairs(rc.ENTRY_PREFILL) == 85_200_896
+    assert L.rows(rc.ROWS_CACHED) == 20_544
+    P = rc.Layout(segs, "paper")
+    n_r, n_st, s = 20480, 64, 4608
+    assert P.pairs(rc.ENTRY_PREFILL) == oc.c_pre(n_r, n_st)
+    assert P.pairs(rc.ENTRY_STEP) == oc.c_step(n_r, s)
+    D = rc.Layout(segs[1:], "dense")
+    assert D.pairs(rc.ENTRY_FULL) * 40 == oc.c_full(n_r, s, 40)
+
+
+def test_live_text_mask_rejected_for_cached_entries():
+    kinds = [0, 1, 2, 3]
+    L = rc.Layout(list(zip(kinds, [4, 4, 4, 4])), om.live_text_mask(kinds))
+    assert L.validate(rc.ENTRY_PREFILL) == rc.RC_ERR_MASK_NOT_CACHEABLE
+    assert L.validate(rc.ENTRY_STEP) == rc.RC_ERR_MASK_NOT_CACHEABLE
+    assert L.validate(rc.ENTRY_FULL) == rc.RC_OK
+    with pytest.raises(rc.RcError) as e:
+        L.pairs(rc.ENTRY_STEP)
+    assert e.value.status == rc.RC_ERR_MASK_NOT_CACHEABLE
+    assert "not exactly cacheable" in rc.lib().rc_last_error().decode()
+
+
+def _prefill(L, B=1, H=2, D=128, scale=0.1, q=FAKE, k=FAKE, v=FAKE, ts=None, o=FAKE, lse=None, kc=FAKE, vc=FAKE):
+    ts = H * D if ts is None else ts
+    return rc.lib().rc_ref_kv_prefill(ctypes.byref(L.c), B, H, D, scale, q, k, v, ts, o, lse, kc, vc, None)
+
+
+def _step(L, B=1, H=2, D=128, scale=0.1, q=FAKE, k=FAKE, v=FAKE, ts=None, kc=FAKE, vc=FAKE, o=FAKE, lse=None,
+          splits=1, ws=None, wsb=0):
+    ts = H * D if ts is None else ts
+    return rc.lib().rc_step_masked_attention(ctypes.byref(L.c), B, H, D, scale, q, k, v, ts, kc, vc, o, lse,
+                                             splits, ws, wsb, None)
+
+
+def _full(L, B=1, H=2, D=128, scale=0.1, q=FAKE, k=FAKE, v=FAKE, ts=None, o=FAKE, lse=None):
+    ts = H * D if ts is None else ts
+    return rc.lib().rc_full_attention(ctypes.byref(L.c), B, H, D, scale, q, k, v, ts, o, lse, None)
+
+
+SEGS = [(0, 8), (1, 16), (2, 64), (3, 64)]
+
+
+def test_argument_errors_launch_nothing():
+    L = rc.Layout(SEGS, "perref")
+    A, U, W = rc.RC_ERR_ARG, rc.RC_ERR_UNSUPPORTED, rc.RC_ERR_WORKSPACE
+    for fn in (_prefill, _step, _full):
+        assert fn(L, q=None) == A
+        assert fn(L, q=FAKE + 8) == A                  # misaligned
+        assert fn(L, o=None) == A
+        assert fn(L, D=96) == U
+        assert fn(L, D=256) == U
+        assert fn(L, B=0) == A
+        assert fn(L, H=0) == A
+        assert fn(L, scale=0.0) == A
+        assert fn(L, scale=float("nan")) == A
+        assert fn(L, ts=2 * 128 - 8) == A              # token stride below H*D
+        assert fn(L, ts=2 * 128 + 4) == A              # not a multiple of 8
+        assert fn(L, lse=FAKE + 2) == A                # misaligned LSE
+        assert rc.lib().rc_last_error().decode() != ""
+    assert _prefill(L, kc=None) == A
+    assert _step(L, vc=None) == A
+    assert _step(L, splits=-1) == A
+    assert _step(L, splits=33) == A
+    assert _step(L, splits=2) == W                     # no workspace
+    need = L.workspace_bytes(1, 2, 128, 2)
+    assert need == 2 * 1 * 2 * 80 * 130 * 4
+    assert _step(L, splits=2, ws=FAKE, wsb=need - 1) == W
+    assert _step(L, splits=2, ws=FAKE + 4, wsb=need) == W
+    # grid overflow: 65535 x 65535 x tiles work-groups
+    assert _full(L, B=65535, H=65535, ts=65535 * 128) == A
+
+
+def test_layout_errors():
+    c = binding.rc_layout()
+    c.n_seg = 0
+    lb = rc.lib()
+    assert lb.rc_layout_preset(ctypes.byref(c), 0) == rc.RC_ERR_ARG
+    assert lb.rc_pairs(ctypes.byref(c), 2) == rc.RC_ERR_ARG
+    c.n_seg = 33
+    assert lb.rc_layout_validate(ctypes.byref(c), 2) == rc.RC_ERR_ARG
+    c.n_seg = 2
+    c.seg[0].kind, c.seg[0].len = 0, 4
+    c.seg[1].kind, c.seg[1].len = 3, 0
+    assert lb.rc_layout_validate(ctypes.byref(c), 2) == rc.RC_ERR_ARG      # zero-length segment
+    c.seg[1].len = 4
+    c.seg[1].kind = 9
+    assert lb.rc_layout_validate(ctypes.byref(c), 2) == rc.RC_ERR_ARG      # unknown kind
+    c.seg[1].kind = 3
+    assert lb.rc_layout_preset(ctypes.byref(c), 7) == rc.RC_ERR_ARG       # unknown preset
+    assert lb.rc_layout_preset(ctypes.byref(c), 1) == rc.RC_OK
+    c.visible[0] |= 1 << 5                                                 # bit beyond n_seg
+    assert lb.rc_layout_validate(ctypes.byref(c), 2) == rc.RC_ERR_ARG
+    assert lb.rc_layout_validate(ctypes.byref(c), 5) == rc.RC_ERR_ARG      # unknown entry
+    assert lb.rc_status_string(rc.RC_ERR_MASK_NOT_CACHEABLE).decode() == "mask is not cacheable"
+
+
+def test_no_rows_is_a_no_op():
+    # a layout without live segments has nothing to step; without static ones nothing to prefill
+    only_static = rc.Layout([(0, 4), (3, 8)], "perref")
+    assert _step(only_static, q=None, k=None, v=None, o=None) == rc.RC_OK
+    only_live = rc.Layout([(1, 4), (2, 8)], "perref")
+    assert _prefill(only_live, q=None, k=None, v=None, o=None, kc=None, vc=None) == rc.RC_OK
+
+
+def test_fragmented_schedule_is_refused():
+    # 32 one-token segments; every query reads the even segments (16 separate
+    # runs) and odd queries also read themselves: 16 distinct lists of 15
+    # runs plus one shared list of 16 -> 256 merged ranges, above the limit
+    segs = [(1, 1)] * 32
+    vis = [[k % 2 == 0 or (q % 2 == 1 and k == q) for k in range(32)] for q in range(32)]
+    L = rc.Layout(segs, vis)
+    assert _full(L) == rc.RC_ERR_UNSUPPORTED
+    assert "merged key ranges" in rc.lib().rc_last_error().decode()
+
+
+def test_auto_splits_and_workspace():
+    L = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
+    assert L.auto_splits(1, 24, 128) == 1            # 864 query tiles already fill the chip
+    assert L.workspace_bytes(1, 24, 128, 0) == 0
+    s = L.auto_splits(1, 3, 128)                      # one GPU's share of 24 heads over 8
+    assert s > 1
+    assert L.workspace_bytes(1, 3, 128, 0) == s * 3 * 4608 * 130 * 4
