@@ -45,8 +45,14 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr int kThreads = 256;
 constexpr float kLazyThreshold = 8.0f;  // log2 units: rescale when a row max grows by > 2^8
 
+// 16-byte-granule XOR swizzle of a K/V tile row.  Bits 0-1 of the row move to
+// bits 2-3 of the granule and bits 2-3 of the row to bits 0-1: any 16
+// consecutive rows at one granule hit 16 distinct granule slots (128-bit K
+// reads), and 4 consecutive rows x 4 consecutive granules hit 16 distinct
+// slots (transpose V reads of two 16-lane groups), so neither access pattern
+// conflicts in the 64-bank LDS.
 __device__ __forceinline__ int swz(int row, int g, int gr) {
-  return g ^ ((((row & 7) << 1) | ((row >> 3) & 1)) & (gr - 1));
+  return g ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (gr - 1));
 }
 
 __device__ __forceinline__ float max_halves(float x) {
@@ -83,58 +89,129 @@ __device__ __forceinline__ void cursor_next(const Params& p, Cursor& c) {
   }
 }
 
-template <int D>
-struct TileRegs {
-  static constexpr int kLoads = kBN * (D / 8) / kThreads;  // 16-byte granules per thread
-  u32x4 k[kLoads];
-  u32x4 v[kLoads];
-};
+typedef __attribute__((address_space(3))) void lds_void;
 
+// Issue the direct global->LDS loads of one K/V tile.  The tile is
+// kBN rows x D/8 granules; wave w's instruction i fills the 1 KB LDS chunk
+// c = i*4 + w, lane l writing granule position p = 64c + l (the hardware puts
+// lane l's 16 bytes at chunk base + 16 l).  Position p holds row p / (D/8),
+// swizzled slot p % (D/8); the per-lane byte offsets `voff` are fixed for
+// the whole kernel.  Rows past the range end lie beyond the buffer record
+// count and read as zeros.  Returns the number of valid rows.
 template <int D>
-__device__ __forceinline__ void load_tile(const Params& p, const Cursor& c, int b, int h, int tid,
-                                          TileRegs<D>& regs, int& valid) {
-  constexpr int GR = D / 8;
-  const KeyRange& rg = p.range[c.r];
-  const KeySrc& s = p.src[rg.src];
+__device__ __forceinline__ int issue_tile(const Params& p, const Cursor& c, int b, int h, int wave,
+                                          const uint32_t* voff0, const uint32_t* voff1, uint16_t* ks,
+                                          uint16_t* vs) {
+  constexpr int kLoads = kBN * (D / 8) / kThreads;
+  const KeyRange rg = p.range[c.r];
+  const uint32_t* voff = rg.src == 0 ? voff0 : voff1;
+  const KeySrc s = p.src[rg.src];
   const int key0 = rg.start + c.t * kBN;
-  valid = min(kBN, rg.len - c.t * kBN);
+  const int valid = min(kBN, rg.len - c.t * kBN);
   const int64_t base = int64_t(b) * s.sb + int64_t(h) * s.sh + int64_t(key0) * s.st;
+  const int nrec = int(int64_t(valid) * s.st * 2);
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(s.k + base), (short)0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(s.v + base), (short)0, nrec, 0x00020000);
 #pragma unroll
-  for (int i = 0; i < TileRegs<D>::kLoads; ++i) {
-    const int gi = tid + kThreads * i;
-    const int row = gi / GR, g = gi % GR;
-    if (row < valid) {
-      const int64_t off = base + int64_t(row) * s.st + g * 8;
-      regs.k[i] = *reinterpret_cast<const u32x4*>(s.k + off);
-      regs.v[i] = *reinterpret_cast<const u32x4*>(s.v + off);
-    } else {
-      regs.k[i] = u32x4{0u, 0u, 0u, 0u};
-      regs.v[i] = u32x4{0u, 0u, 0u, 0u};
+  for (int i = 0; i < kLoads; ++i) {
+    const int chunk = i * 4 + wave;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(ks + chunk * 512), 16, voff[i], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vs + chunk * 512), 16, voff[i], 0, 0, 0);
+  }
+  return valid;
+}
+
+// One 64-key tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
+template <int D>
+__device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t* vs, int lane, int valid,
+                                             const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
+                                             float& lsum, float c) {
+  constexpr int GR = D / 8;
+  constexpr int NDC = D / 16;
+  constexpr int NB = D / 32;
+  const int hh = lane >> 5;
+  f32x16 sacc[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+    const int krow = kb * 32 + (lane & 31);
+#pragma unroll
+    for (int dc = 0; dc < NDC; ++dc) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + hh, GR) * 8);
+      sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[dc], sacc[kb], 0, 0, 0);
+    }
+  }
+  // ragged tail: keys past the end of the range score -inf
+  if (valid < kBN) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (key >= valid) sacc[kb][r] = -INFINITY;
+      }
+  }
+  // online softmax (row = this lane's query)
+  float mx = sacc[0][0];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+  const float mt = max_halves(mx) * c;
+  if (__any(mt > m_used + kLazyThreshold)) {
+    const float m_new = fmaxf(m_used, mt);
+    const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
+    lsum *= alpha;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
+    m_used = m_new;
+  }
+  bf16x8 pf[4];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
+      lsum += e;
+      pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
+    }
+  // O^T += V^T P^T: 16 keys per MFMA, 32 d-rows per MFMA
+  const int grp = lane >> 4, li = lane & 15;
+  const int dhalf = grp & 1;
+  const int rsub = li >> 2, dsub = 4 * (li & 3);
+#pragma unroll
+  for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int d = nb * 32 + dhalf * 16 + dsub;
+      const int r0 = cc * 16 + 4 * hh + rsub;
+      const int r1 = r0 + 8;
+      const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
+      const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
+      typedef short i16x8 __attribute__((ext_vector_type(8)));
+      const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pf[cc], oacc[nb], 0, 0, 0);
     }
   }
 }
 
-template <int D>
-__device__ __forceinline__ void store_tile(uint16_t* ks, uint16_t* vs, int tid, const TileRegs<D>& regs) {
-  constexpr int GR = D / 8;
-#pragma unroll
-  for (int i = 0; i < TileRegs<D>::kLoads; ++i) {
-    const int gi = tid + kThreads * i;
-    const int row = gi / GR, g = gi % GR;
-    const int off = row * D + swz(row, g, GR) * 8;
-    *reinterpret_cast<u32x4*>(ks + off) = regs.k[i];
-    *reinterpret_cast<u32x4*>(vs + off) = regs.v[i];
-  }
-}
+__device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 template <int D, bool kSplit>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   constexpr int GR = D / 8;
   constexpr int NDC = D / 16;  // 16-wide d chunks of the QK^T contraction
   constexpr int NB = D / 32;   // 32-wide d blocks of the output
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2][2][kBN * D];
+  constexpr int kLoads = kBN * GR / kThreads;
+  __shared__ __attribute__((aligned(1024))) uint16_t k0[kBN * D], v0[kBN * D], k1[kBN * D], v1[kBN * D];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5;  // which 32-lane half
 
   // ---- work item: XCD-aware remap so consecutive logical items (same head)
@@ -156,6 +233,28 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   const int row0 = qs.row0 + seg_row0;  // first row of the tile in the Q/O buffers
   const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
   const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+
+  // per-lane byte offsets of this lane's granules inside a tile (same for K and V)
+  uint32_t voff[kLoads];
+  {
+    const KeySrc s0 = p.src[0];
+    const KeySrc s1 = p.src[1];
+    (void)s1;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int pos = (i * 4 + wave) * 64 + lane;
+      const int row = pos / GR, slot = pos % GR;
+      voff[i] = uint32_t(row) * uint32_t(s0.st) * 2u + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+    }
+  }
+  // the two key sources may have different token strides: offsets for source 1
+  uint32_t voff1[kLoads];
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) {
+    const int pos = (i * 4 + wave) * 64 + lane;
+    const int row = pos / GR, slot = pos % GR;
+    voff1[i] = uint32_t(row) * uint32_t(p.src[1].st) * 2u + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+  }
 
   // ---- Q fragment (B operand of S^T = K Q^T): lane holds query (lane % 32),
   // d = 16*dc + 8*hh .. +7.
@@ -180,101 +279,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   float lsum = 0.f;          // this half's partial row sum
   const float c = p.scale_log2;
 
-  TileRegs<D> regs;
   Cursor cur = cursor_at(p, qs, kt_begin);
-  int valid_cur = 0, valid_next = 0;
-  if (kt_begin < kt_end) {
-    load_tile<D>(p, cur, b, h, tid, regs, valid_cur);
-    store_tile<D>(smem[0][0], smem[0][1], tid, regs);
-  }
-  __syncthreads();
-
-  for (int kt = kt_begin; kt < kt_end; ++kt) {
-    const int stage = (kt - kt_begin) & 1;
-    const bool more = kt + 1 < kt_end;
-    Cursor nxt = cur;
-    if (more) {
-      cursor_next(p, nxt);
-      load_tile<D>(p, nxt, b, h, tid, regs, valid_next);
-    }
-    const uint16_t* ks = smem[stage][0];
-    const uint16_t* vs = smem[stage][1];
-
-    // ---- S^T = K Q^T for 64 keys: two 32-key blocks
-    f32x16 sacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-      const int krow = kb * 32 + (lane & 31);
-#pragma unroll
-      for (int dc = 0; dc < NDC; ++dc) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + hh, GR) * 8);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[dc], sacc[kb], 0, 0, 0);
-      }
-    }
-    // ragged tail: keys past the end of the range score -inf
-    if (valid_cur < kBN) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          if (key >= valid_cur) sacc[kb][r] = -INFINITY;
-        }
-    }
-    // ---- online softmax (row = this lane's query)
-    float mx = sacc[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-    const float mt = max_halves(mx) * c;
-    if (__any(mt > m_used + kLazyThreshold)) {
-      const float m_new = fmaxf(m_used, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
-      lsum *= alpha;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
-      m_used = m_new;
-    }
-    bf16x8 pf[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
-        lsum += e;
-        pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
-      }
-    // ---- O^T += V^T P^T: 16 keys per MFMA, 32 d-rows per MFMA
-    {
-      const int grp = lane >> 4, li = lane & 15;
-      const int dhalf = grp & 1;
-      const int rsub = li >> 2, dsub = 4 * (li & 3);
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int d = nb * 32 + dhalf * 16 + dsub;
-          const int r0 = cc * 16 + 4 * hh + rsub;
-          const int r1 = r0 + 8;
-          const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
-          const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
-          typedef short i16x8 __attribute__((ext_vector_type(8)));
-          const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pf[cc], oacc[nb], 0, 0, 0);
-        }
-      }
-    }
-    if (more) store_tile<D>(smem[stage ^ 1][0], smem[stage ^ 1][1], tid, regs);
+  int valid_cur = 0;
+  if (kt_begin < kt_end) valid_cur = issue_tile<D>(p, cur, b, h, wave, voff, voff1, k0, v0);
+  for (int kt = kt_begin; kt < kt_end; kt += 2) {
+    // even tile in buffer 0; prefetch the next one into buffer 1
+    wait_tile_loads();
     __syncthreads();
+    Cursor nxt = cur;
+    int valid_nxt = 0;
+    const bool more1 = kt + 1 < kt_end;
+    if (more1) {
+      cursor_next(p, nxt);
+      valid_nxt = issue_tile<D>(p, nxt, b, h, wave, voff, voff1, k1, v1);
+    }
+    tile_compute<D>(k0, v0, lane, valid_cur, qf, oacc, m_used, lsum, c);
+    if (!more1) break;
     cur = nxt;
-    valid_cur = valid_next;
+    valid_cur = valid_nxt;
+    // odd tile in buffer 1; prefetch the next one into buffer 0
+    wait_tile_loads();
+    __syncthreads();
+    const bool more2 = kt + 2 < kt_end;
+    if (more2) {
+      cursor_next(p, nxt);
+      valid_nxt = issue_tile<D>(p, nxt, b, h, wave, voff, voff1, k0, v0);
+    }
+    tile_compute<D>(k1, v1, lane, valid_cur, qf, oacc, m_used, lsum, c);
+    cur = nxt;
+    valid_cur = valid_nxt;
   }
 
   // ---- epilogue
