@@ -42,7 +42,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kThreads = 256;
 constexpr float kLazyThreshold = 8.0f;  // log2 units: rescale when a row max grows by > 2^8
 
 // 16-byte-granule XOR swizzle of a K/V tile row.  Bits 0-1 of the row move to
@@ -91,20 +90,71 @@ __device__ __forceinline__ void cursor_next(const Params& p, Cursor& c) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+constexpr int kThreads = 64 * kWaves;
+constexpr int kTileElems = kBN * 128;  // LDS elements reserved per K or V tile (D <= 128)
+
+// The K/V ring in LDS.  Separate objects per stage (selected at compile time)
+// let the compiler see that a DMA into one stage never aliases reads of
+// another, so it inserts no conservative vector-memory waits before them.
+__shared__ __attribute__((aligned(1024))) uint16_t g_k0[kTileElems];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v0[kTileElems];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k1[kTileElems];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v1[kTileElems];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k2[kStages > 2 ? kTileElems : 8];
+__shared__ __attribute__((aligned(1024))) uint16_t g_v2[kStages > 2 ? kTileElems : 8];
+
+template <int S>
+__device__ __forceinline__ uint16_t* kbuf() {
+  if constexpr (S == 0) return g_k0;
+  else if constexpr (S == 1) return g_k1;
+  else return g_k2;
+}
+template <int S>
+__device__ __forceinline__ uint16_t* vbuf() {
+  if constexpr (S == 0) return g_v0;
+  else if constexpr (S == 1) return g_v1;
+  else return g_v2;
+}
+
+// Work-group barrier without the memory fences of __syncthreads(): every
+// wave first waits for its own LDS reads; the tile DMA is waited for
+// explicitly (wait_tiles_in_flight) so that later tiles stay in flight.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+}
+
+// 32-bit LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* ptr) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void*)ptr));
+}
+
+// One 16-byte-per-lane buffer load straight into LDS: lane l's bytes land at
+// M0 + 16 l; offsets past the buffer's record count read as zeros.  Written
+// as inline assembly so the compiler does no alias tracking of its own for
+// these LDS writes (it would otherwise wait for every in-flight tile before
+// unrelated LDS reads); the kernel waits for the loads explicitly with
+// vmcnt.  M0 needs one wait state before the load.
+__device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, __amdgpu_buffer_rsrc_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+
 // Issue the direct global->LDS loads of one K/V tile.  The tile is
-// kBN rows x D/8 granules; wave w's instruction i fills the 1 KB LDS chunk
-// c = i*4 + w, lane l writing granule position p = 64c + l (the hardware puts
-// lane l's 16 bytes at chunk base + 16 l).  Position p holds row p / (D/8),
-// swizzled slot p % (D/8); the per-lane byte offsets `voff` are fixed for
-// the whole kernel.  Rows past the range end lie beyond the buffer record
-// count and read as zeros.  Returns the number of valid rows.
+// kBN rows x D/8 16-byte granules; wave w's instruction i fills the 1 KB LDS
+// chunk c = i * kWaves + w, lane l writing granule position p = 64 c + l (the
+// hardware puts lane l's 16 bytes at chunk base + 16 l).  Position p holds
+// row p / (D/8), swizzled slot p % (D/8); the per-lane byte offsets `voff`
+// are fixed for the whole kernel.  Rows past the range end lie beyond the
+// buffer record count and arrive as zeros.
 template <int D>
-__device__ __forceinline__ int issue_tile(const Params& p, const Cursor& c, int b, int h, int wave,
-                                          const uint32_t* voff0, const uint32_t* voff1, uint16_t* ks,
-                                          uint16_t* vs) {
+__device__ __forceinline__ void issue_tile(const Params& p, const Cursor& c, int b, int h, int wave,
+                                           const uint32_t* voff0, const uint32_t* voff1, uint16_t* ks,
+                                           uint16_t* vs) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
   const KeyRange rg = p.range[c.r];
-  const uint32_t* voff = rg.src == 0 ? voff0 : voff1;
   const KeySrc s = p.src[rg.src];
   const int key0 = rg.start + c.t * kBN;
   const int valid = min(kBN, rg.len - c.t * kBN);
@@ -112,13 +162,27 @@ __device__ __forceinline__ int issue_tile(const Params& p, const Cursor& c, int 
   const int nrec = int(int64_t(valid) * s.st * 2);
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(s.k + base), (short)0, nrec, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(s.v + base), (short)0, nrec, 0x00020000);
+  // the lane offsets are passed straight from the long-lived per-source
+  // registers (a uniform branch, not a select into a temporary)
+  if (rg.src == 0) {
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int chunk = i * 4 + wave;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(ks + chunk * 512), 16, voff[i], 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vs + chunk * 512), 16, voff[i], 0, 0, 0);
+    for (int i = 0; i < kLoads; ++i) {
+      const int chunk = i * kWaves + wave;
+      dma16(lds_addr(ks + chunk * 512), voff0[i], rk);
+      dma16(lds_addr(vs + chunk * 512), voff0[i], rv);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int chunk = i * kWaves + wave;
+      dma16(lds_addr(ks + chunk * 512), voff1[i], rk);
+      dma16(lds_addr(vs + chunk * 512), voff1[i], rv);
+    }
   }
-  return valid;
+}
+
+__device__ __forceinline__ int tile_valid(const Params& p, const Cursor& c) {
+  return min(kBN, p.range[c.r].len - c.t * kBN);
 }
 
 // One 64-key tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
@@ -200,15 +264,56 @@ __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t*
   }
 }
 
-__device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most `n` tiles of this wave's DMA loads are still in flight
+// (each tile is 2 * kLoads vector-memory instructions per wave).
+template <int kLoads>
+__device__ __forceinline__ void wait_tiles_in_flight(int n) {
+  static_assert(2 * kLoads * (kStages - 1) <= 63, "vmcnt range");
+  if (n <= 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else if (n == 1) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads) : "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * 2) : "memory");
+  }
+}
+
+// State a wave carries through the K/V ring.
+template <int D>
+struct RingState {
+  Cursor icur, ccur;  // next tile to issue, next tile to compute
+  int issued;         // tiles issued so far (absolute key-tile index)
+};
+
+// Tile k (in stage S): wait for its DMA, barrier, refill the stage that
+// became free with tile k + kStages - 1, then compute tile k.
+template <int S, int D>
+__device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, int b, int h, int wave, int lane,
+                                          bool wave_active, const uint32_t* voff0, const uint32_t* voff1,
+                                          RingState<D>& rs, const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
+                                          float& m_used, float& lsum, float c) {
+  constexpr int kLoads = kBN * (D / 8) / kThreads;
+  constexpr int F = (S + kStages - 1) % kStages;  // stage freed by the previous tile
+  wait_tiles_in_flight<kLoads>(rs.issued - 1 - k);
+  ring_barrier();
+  if (rs.issued < kt_end) {
+    issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<F>(), vbuf<F>());
+    ++rs.issued;
+    if (rs.issued < kt_end) cursor_next(p, rs.icur);
+  }
+  const int valid = tile_valid(p, rs.ccur);
+  if (wave_active) tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
+  if (k + 1 < kt_end) cursor_next(p, rs.ccur);
+}
 
 template <int D, bool kSplit>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
+__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   constexpr int GR = D / 8;
   constexpr int NDC = D / 16;  // 16-wide d chunks of the QK^T contraction
   constexpr int NB = D / 32;   // 32-wide d blocks of the output
   constexpr int kLoads = kBN * GR / kThreads;
-  __shared__ __attribute__((aligned(1024))) uint16_t k0[kBN * D], v0[kBN * D], k1[kBN * D], v1[kBN * D];
+  static_assert(kLoads >= 1 && kBN * GR % kThreads == 0, "tile granules must divide over the threads");
+  static_assert(kStages >= 2 && kStages <= 3, "stage ring of 2 or 3 tiles");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -233,27 +338,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   const int row0 = qs.row0 + seg_row0;  // first row of the tile in the Q/O buffers
   const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
   const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+  const bool wave_active = wave * 32 < rows_valid;  // wave-uniform
 
-  // per-lane byte offsets of this lane's granules inside a tile (same for K and V)
-  uint32_t voff[kLoads];
-  {
-    const KeySrc s0 = p.src[0];
-    const KeySrc s1 = p.src[1];
-    (void)s1;
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int pos = (i * 4 + wave) * 64 + lane;
-      const int row = pos / GR, slot = pos % GR;
-      voff[i] = uint32_t(row) * uint32_t(s0.st) * 2u + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
-    }
-  }
-  // the two key sources may have different token strides: offsets for source 1
-  uint32_t voff1[kLoads];
+  // per-lane byte offsets of this lane's granules inside a tile, per key source
+  uint32_t voff0[kLoads], voff1[kLoads];
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
-    const int pos = (i * 4 + wave) * 64 + lane;
+    const int pos = (i * kWaves + wave) * 64 + lane;
     const int row = pos / GR, slot = pos % GR;
-    voff1[i] = uint32_t(row) * uint32_t(p.src[1].st) * 2u + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+    const uint32_t g16 = uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+    voff0[i] = uint32_t(row) * uint32_t(p.src[0].st) * 2u + g16;
+    voff1[i] = uint32_t(row) * uint32_t(p.src[1].st) * 2u + g16;
   }
 
   // ---- Q fragment (B operand of S^T = K Q^T): lane holds query (lane % 32),
@@ -269,6 +364,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
       qf[dc] = __builtin_bit_cast(bf16x8, raw);
     }
   }
+  // Q in registers before any tile DMA is counted; a compiler-visible wait
+  // (gfx9 encoding of vmcnt(0) with expcnt/lgkmcnt left at their maxima) so
+  // that no further waits for these loads are inserted inside the loop
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 
   f32x16 oacc[NB];
 #pragma unroll
@@ -279,35 +378,31 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   float lsum = 0.f;          // this half's partial row sum
   const float c = p.scale_log2;
 
-  Cursor cur = cursor_at(p, qs, kt_begin);
-  int valid_cur = 0;
-  if (kt_begin < kt_end) valid_cur = issue_tile<D>(p, cur, b, h, wave, voff, voff1, k0, v0);
-  for (int kt = kt_begin; kt < kt_end; kt += 2) {
-    // even tile in buffer 0; prefetch the next one into buffer 1
-    wait_tile_loads();
-    __syncthreads();
-    Cursor nxt = cur;
-    int valid_nxt = 0;
-    const bool more1 = kt + 1 < kt_end;
-    if (more1) {
-      cursor_next(p, nxt);
-      valid_nxt = issue_tile<D>(p, nxt, b, h, wave, voff, voff1, k1, v1);
+  // ---- K/V ring: tile kt lives in stage (kt - kt_begin) % kStages; tiles up
+  // to kStages - 1 ahead are in flight while one is computed.
+  RingState<D> rs;
+  rs.icur = cursor_at(p, qs, kt_begin);
+  rs.ccur = rs.icur;
+  rs.issued = kt_begin;
+  if (rs.issued < kt_end) {
+    issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<0>(), vbuf<0>());
+    if (++rs.issued < kt_end) cursor_next(p, rs.icur);
+  }
+  if constexpr (kStages > 2) {
+    if (rs.issued < kt_end) {
+      issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<1>(), vbuf<1>());
+      if (++rs.issued < kt_end) cursor_next(p, rs.icur);
     }
-    tile_compute<D>(k0, v0, lane, valid_cur, qf, oacc, m_used, lsum, c);
-    if (!more1) break;
-    cur = nxt;
-    valid_cur = valid_nxt;
-    // odd tile in buffer 1; prefetch the next one into buffer 0
-    wait_tile_loads();
-    __syncthreads();
-    const bool more2 = kt + 2 < kt_end;
-    if (more2) {
-      cursor_next(p, nxt);
-      valid_nxt = issue_tile<D>(p, nxt, b, h, wave, voff, voff1, k0, v0);
+  }
+  for (int kt = kt_begin; kt < kt_end; kt += kStages) {
+    ring_step<0, D>(p, kt, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
+    if (kt + 1 >= kt_end) break;
+    ring_step<1, D>(p, kt + 1, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
+    if constexpr (kStages > 2) {
+      if (kt + 2 >= kt_end) break;
+      ring_step<2, D>(p, kt + 2, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum,
+                      c);
     }
-    tile_compute<D>(k1, v1, lane, valid_cur, qf, oacc, m_used, lsum, c);
-    cur = nxt;
-    valid_cur = valid_nxt;
   }
 
   // ---- epilogue

@@ -210,9 +210,10 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
 
 int32_t auto_splits(const Params& p) {
   // Split the keys only when the query tiles alone leave the 256 CUs
-  // (two work-groups each) under-filled; keep >= 8 key tiles per split.
+  // under-filled (one 8-wave work-group per CU, or two 4-wave ones); keep
+  // >= 8 key tiles per split.
   const int64_t wgs = int64_t(p.B) * p.H * p.n_qtiles;
-  const int64_t slots = 512;
+  const int64_t slots = 256 * (8 / kWaves);
   if (wgs <= 0 || wgs >= slots) return 1;
   int max_kt = 0;
   for (int i = 0; i < p.n_qseg; ++i)

@@ -16,7 +16,15 @@
 
 namespace rc {
 
-constexpr int kBM = 128;          // query rows per work-group (4 waves x 32)
+#ifndef RC_WAVES
+#define RC_WAVES 8                // waves per work-group, 32 query rows each
+#endif
+#ifndef RC_STAGES
+#define RC_STAGES 2               // K/V tiles resident in LDS (prefetch distance RC_STAGES - 1)
+#endif
+constexpr int kWaves = RC_WAVES;
+constexpr int kStages = RC_STAGES;
+constexpr int kBM = 32 * kWaves;  // query rows per work-group
 constexpr int kBN = 64;           // keys per K/V tile
 constexpr int kMaxRanges = 96;    // merged key ranges over all query segments
 constexpr int kMaxSplits = 32;
