@@ -3,11 +3,12 @@
 //
 // Method: softmax(scale * Q K^T) V over the visible key segments of each
 // query segment (Sec. 3.3 mask; App. C interaction counts).  The planner
-// hands every work-group a BM = 128-row query tile inside one segment and the
-// list of visible key ranges; invisible segments are never loaded.
+// hands every work-group a BM-row query tile inside one segment and the list
+// of visible key ranges; invisible segments are never loaded.
 //
-// Work-group = 4 waves of 64 lanes, each wave owns 32 query rows.  Per 64-key
-// tile:
+// Work-group = kWaves waves of 64 lanes (8 by default: BM = 256 rows, one
+// work-group and two waves per SIMD on each CU); each wave owns 32 query rows.
+// Per 64-key tile:
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = the
 //                   wave's Q rows held in registers for the whole kernel.
 //                   The 32x32 accumulator puts one query per lane (lane % 32)
@@ -22,10 +23,10 @@
 //                   the S^T accumulator registers (bf16), so the output also
 //                   has one query per lane and the softmax statistics never
 //                   leave their lane.
-// K/V tiles are double-buffered in LDS with 16-byte global loads (coalesced:
-// 16 lanes cover one 256-byte row) and an XOR swizzle at 16-byte granularity
-// that keeps both the 128-bit K reads and the transpose V reads free of bank
-// conflicts.
+// K/V tiles stream through a ring of kStages LDS stages (2 by default) with
+// direct global->LDS buffer loads (16 bytes per lane, 16 lanes per 256-byte
+// row), placed with an XOR swizzle at 16-byte granularity that keeps both the
+// 128-bit K reads and the transpose V reads free of bank conflicts.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
