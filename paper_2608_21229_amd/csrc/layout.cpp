@@ -209,16 +209,18 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
 }
 
 int32_t auto_splits(const Params& p) {
-  // Split the keys only when the query tiles alone leave the 256 CUs
-  // under-filled (one 8-wave work-group per CU, or two 4-wave ones); keep
-  // >= 8 key tiles per split.
+  // Split the keys only when the query tiles alone leave CUs idle, and only as
+  // far as one round of work-groups still fits on the 256 CUs: every extra
+  // split costs a Q load, a partial write and its share of the combine, which
+  // measured more than the idle CUs of a partial second round.  Keep >= 8 key
+  // tiles per split.
   const int64_t wgs = int64_t(p.B) * p.H * p.n_qtiles;
   const int64_t slots = 256 * (8 / kWaves);
   if (wgs <= 0 || wgs >= slots) return 1;
   int max_kt = 0;
   for (int i = 0; i < p.n_qseg; ++i)
     if (p.qseg[i].ktiles > max_kt) max_kt = p.qseg[i].ktiles;
-  int64_t s = (2 * slots + wgs - 1) / wgs;
+  int64_t s = slots / wgs;
   const int64_t cap = max_kt / 8;
   if (s > cap) s = cap;
   if (s > kMaxSplits) s = kMaxSplits;

@@ -187,8 +187,13 @@ def test_fragmented_schedule_is_refused():
 
 def test_auto_splits_and_workspace():
     L = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
-    assert L.auto_splits(1, 24, 128) == 1            # 864 query tiles already fill the chip
+    assert L.auto_splits(1, 24, 128) == 1            # 432 query tiles already exceed one round
     assert L.workspace_bytes(1, 24, 128, 0) == 0
-    s = L.auto_splits(1, 3, 128)                      # one GPU's share of 24 heads over 8
-    assert s > 1
-    assert L.workspace_bytes(1, 3, 128, 0) == s * 3 * 4608 * 130 * 4
+    # one GPU's share of 24 heads over 8: 54 query tiles, 4 splits keep one round
+    assert L.auto_splits(1, 3, 128) == 4
+    assert L.workspace_bytes(1, 3, 128, 0) == 4 * 3 * 4608 * 130 * 4
+    assert L.auto_splits(1, 7, 128) == 2             # 126 query tiles
+    assert L.auto_splits(1, 1, 128) == 14            # 18 query tiles
+    # few key tiles cap the splits at one per 8 key tiles
+    L2 = rc.Layout([(1, 64), (2, 64)], "perref")
+    assert L2.auto_splits(1, 1, 128) == 1
