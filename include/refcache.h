@@ -27,7 +27,7 @@
  *                  fp32 for LSE and workspace.  Arithmetic: bf16 products,
  *                  fp32 accumulation and softmax, O rounded to bf16 (RNE).
  *   Token layout   Q/K/V are [B, N, H, D] with D contiguous and head stride D;
- *                  `tok_stride` (elements, >= H*D, multiple of 8) separates
+ *                  `tok_stride` (elements, >= H*D, multiple of 8, <= 2^24) separates
  *                  consecutive tokens so views into a fused QKV buffer work;
  *                  batch stride is N * tok_stride.  O is contiguous
  *                  [B, N, H, D].  LSE is contiguous [B, H, N] (natural log).

@@ -53,8 +53,10 @@ rc_status check_stride(int64_t tok_stride, int32_t H, int32_t D) {
     set_error("tok_stride %lld must be >= H*D = %d and a multiple of 8", (long long)tok_stride, H * D);
     return RC_ERR_ARG;
   }
-  if (tok_stride > (int64_t(1) << 32)) {
-    set_error("tok_stride %lld is too large", (long long)tok_stride);
+  // a 64-token tile of the source spans 128 * tok_stride bytes, addressed
+  // with 32-bit buffer offsets
+  if (tok_stride > (int64_t(1) << 24)) {
+    set_error("tok_stride %lld is too large (at most 2^24 elements)", (long long)tok_stride);
     return RC_ERR_ARG;
   }
   return RC_OK;

@@ -26,7 +26,11 @@
 // K/V tiles stream through a ring of kStages LDS stages (2 by default) with
 // direct global->LDS buffer loads (16 bytes per lane, 16 lanes per 256-byte
 // row), placed with an XOR swizzle at 16-byte granularity that keeps both the
-// 128-bit K reads and the transpose V reads free of bank conflicts.
+// 128-bit K reads and the transpose V reads free of bank conflicts.  The
+// tile cursor keeps the current key range's pointers in scalar registers, so
+// issuing a tile needs no reads of the range table; the K and V fragment
+// reads are software-pipelined kPrefetch MFMAs ahead of their use, and the
+// softmax row max and row sum run as four independent chains.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -66,26 +70,60 @@ __device__ __forceinline__ float sum_halves(float x) {
   return __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
 }
 
-// Cursor over the key tiles of one query segment: (range, tile inside range).
+// Cursor over the key tiles of one query segment.  It keeps the current key
+// range's source pointers, stride and remaining key count in (scalar)
+// registers and steps from tile to tile by pointer arithmetic; the range and
+// source descriptors in the kernel arguments are read again only when the
+// cursor crosses into the next range.
 struct Cursor {
-  int r, t;
+  const uint16_t* k;  // K / V of the current tile's first key, batch and head applied
+  const uint16_t* v;
+  int64_t step;       // elements between consecutive tiles of the range (kBN * st)
+  int32_t st;         // token stride of the key source (elements)
+  int32_t rem;        // keys of the range from the current tile on
+  int32_t src;        // key source of the range
+  int32_t r, t, ntiles, r_end;
+  int32_t b, h;
 };
 
-__device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int kt) {
-  Cursor c{qs.r0, kt};
-  for (int i = 0; i < qs.nr; ++i) {
-    const int n = p.range[qs.r0 + i].ntiles;
-    if (c.t < n) break;
-    c.t -= n;
-    ++c.r;
+__device__ __forceinline__ void cursor_load(const Params& p, Cursor& c, int r, int t) {
+  const KeyRange rg = p.range[r];
+  const KeySrc s = p.src[rg.src];
+  c.r = r;
+  c.t = t;
+  c.ntiles = rg.ntiles;
+  c.src = rg.src;
+  c.st = int32_t(s.st);
+  c.rem = rg.len - t * kBN;
+  c.step = int64_t(kBN) * s.st;
+  const int64_t base = int64_t(c.b) * s.sb + int64_t(c.h) * s.sh + int64_t(rg.start + t * kBN) * s.st;
+  c.k = s.k + base;
+  c.v = s.v + base;
+}
+
+__device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int kt, int b, int h) {
+  Cursor c;
+  c.b = b;
+  c.h = h;
+  c.r_end = qs.r0 + qs.nr;
+  int r = qs.r0;
+  for (int i = 0; i + 1 < qs.nr; ++i) {
+    const int n = p.range[r].ntiles;
+    if (kt < n) break;
+    kt -= n;
+    ++r;
   }
+  cursor_load(p, c, r, kt);
   return c;
 }
 
 __device__ __forceinline__ void cursor_next(const Params& p, Cursor& c) {
-  if (++c.t >= p.range[c.r].ntiles) {
-    c.t = 0;
-    ++c.r;
+  if (++c.t < c.ntiles) {
+    c.k += c.step;
+    c.v += c.step;
+    c.rem -= kBN;
+  } else if (c.r + 1 < c.r_end) {
+    cursor_load(p, c, c.r + 1, 0);
   }
 }
 
@@ -151,21 +189,16 @@ __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, __amdgpu_buff
 // are fixed for the whole kernel.  Rows past the range end lie beyond the
 // buffer record count and arrive as zeros.
 template <int D>
-__device__ __forceinline__ void issue_tile(const Params& p, const Cursor& c, int b, int h, int wave,
-                                           const uint32_t* voff0, const uint32_t* voff1, uint16_t* ks,
-                                           uint16_t* vs) {
+__device__ __forceinline__ void issue_tile(const Cursor& c, int wave, const uint32_t* voff0, const uint32_t* voff1,
+                                           uint16_t* ks, uint16_t* vs) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
-  const KeyRange rg = p.range[c.r];
-  const KeySrc s = p.src[rg.src];
-  const int key0 = rg.start + c.t * kBN;
-  const int valid = min(kBN, rg.len - c.t * kBN);
-  const int64_t base = int64_t(b) * s.sb + int64_t(h) * s.sh + int64_t(key0) * s.st;
-  const int nrec = int(int64_t(valid) * s.st * 2);
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(s.k + base), (short)0, nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(s.v + base), (short)0, nrec, 0x00020000);
+  const int valid = min(kBN, c.rem);
+  const int nrec = valid * c.st * 2;
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
   // the lane offsets are passed straight from the long-lived per-source
   // registers (a uniform branch, not a select into a temporary)
-  if (rg.src == 0) {
+  if (c.src == 0) {
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
       const int chunk = i * kWaves + wave;
@@ -182,47 +215,90 @@ __device__ __forceinline__ void issue_tile(const Params& p, const Cursor& c, int
   }
 }
 
-__device__ __forceinline__ int tile_valid(const Params& p, const Cursor& c) {
-  return min(kBN, p.range[c.r].len - c.t * kBN);
+__device__ __forceinline__ int tile_valid(const Cursor& c) { return min(kBN, c.rem); }
+
+#ifndef RC_PREFETCH
+#define RC_PREFETCH 3  // LDS fragment reads kept in flight ahead of the MFMA that uses them
+#endif
+constexpr int kPrefetch = RC_PREFETCH;
+#ifndef RC_ILP
+#define RC_ILP 1  // split the softmax max and sum into independent chains
+#endif
+
+// Scheduling fence: the compiler moves no instruction across it, so the
+// software-pipelined order below (reads issued kPrefetch MFMAs ahead) stays.
+__device__ __forceinline__ void sched_fence() {
+  if constexpr (kPrefetch > 0) __builtin_amdgcn_sched_barrier(0);
 }
 
-// One 64-key tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
+// K fragment f = kb * NDC + dc of S^T = K Q^T: rows kb*32 + lane%32,
+// granule 2 dc + lane/32.
 template <int D>
-__device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t* vs, int lane, int valid,
-                                             const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
-                                             float& lsum, float c) {
+__device__ __forceinline__ bf16x8 k_frag(const uint16_t* ks, int lane, int f) {
   constexpr int GR = D / 8;
   constexpr int NDC = D / 16;
-  constexpr int NB = D / 32;
-  const int hh = lane >> 5;
-  f32x16 sacc[2];
+  const int kb = f / NDC, dc = f % NDC;
+  const int krow = kb * 32 + (lane & 31);
+  return *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + (lane >> 5), GR) * 8);
+}
+
+// S^T = K Q^T for one 64-key tile (two 32x32 accumulators).
+template <int D>
+__device__ __forceinline__ void s_part(const uint16_t* ks, int lane, const bf16x8 (&qf)[D / 16],
+                                       f32x16 (&sacc)[2]) {
+  constexpr int NDC = D / 16;
+  constexpr int NF = 2 * NDC;
+  constexpr int PF = kPrefetch > 0 ? kPrefetch : 1;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-    const int krow = kb * 32 + (lane & 31);
+  bf16x8 a[PF + 1];
 #pragma unroll
-    for (int dc = 0; dc < NDC; ++dc) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + hh, GR) * 8);
-      sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[dc], sacc[kb], 0, 0, 0);
-    }
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = k_frag<D>(ks, lane, f);
+  sched_fence();
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int kb = f / NDC, dc = f % NDC;
+    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], qf[dc], sacc[kb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = k_frag<D>(ks, lane, f + PF);
+    sched_fence();
   }
-  // ragged tail: keys past the end of the range score -inf
+}
+
+// Online softmax of one S^T tile (row = this lane's query) into P^T (bf16).
+template <int D>
+__device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)[2], bf16x8 (&pf)[4],
+                                             f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float c) {
+  constexpr int NB = D / 32;
+  const int hh = lane >> 5;
+  // ragged tail: keys past the end of the range score -inf.  Slot r of half
+  // hh holds key kb*32 + 8 (r/4) + 4 hh + r%4: compare the lane-independent
+  // part against valid - 4 hh.
   if (valid < kBN) {
+    const int lim = valid - 4 * hh;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        if (key >= valid) sacc[kb][r] = -INFINITY;
-      }
+      for (int r = 0; r < 16; ++r)
+        if (kb * 32 + 8 * (r >> 2) + (r & 3) >= lim) sacc[kb][r] = -INFINITY;
   }
-  // online softmax (row = this lane's query)
+#if RC_ILP
+  // four independent max chains (a single wave has no other wave's work to
+  // hide the latency of one serial chain behind)
+  float mq[4] = {sacc[0][0], sacc[0][1], sacc[0][2], sacc[0][3]};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = (kb == 0 ? 4 : 0); r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], sacc[kb][r]);
+  const float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+#else
   float mx = sacc[0][0];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+#endif
   const float mt = max_halves(mx) * c;
   if (__any(mt > m_used + kLazyThreshold)) {
     const float m_new = fmaxf(m_used, mt);
@@ -234,7 +310,19 @@ __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t*
       for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
     m_used = m_new;
   }
-  bf16x8 pf[4];
+#if RC_ILP
+  // four independent partial sums, added to the running sum once per tile
+  float lq[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
+      lq[r & 3] += e;
+      pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
+    }
+  lsum += (lq[0] + lq[1]) + (lq[2] + lq[3]);
+#else
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -243,26 +331,60 @@ __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t*
       lsum += e;
       pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
     }
-  // O^T += V^T P^T: 16 keys per MFMA, 32 d-rows per MFMA
-  const int grp = lane >> 4, li = lane & 15;
-  const int dhalf = grp & 1;
-  const int rsub = li >> 2, dsub = 4 * (li & 3);
+#endif
+}
+
+// V^T fragment f = cc * NB + nb of O^T += V^T P^T: two transpose reads of V
+// rows 16 cc + 4 (lane/32) + (lane%16)/4 (and 8 rows further) at
+// d = 32 nb + 16 ((lane/16)&1) + 4 (lane%4) .. +3, matching the key order of
+// P^T in the S^T accumulator.
+template <int D>
+__device__ __forceinline__ bf16x8 v_frag(const uint16_t* vs, int lane, int f) {
+  constexpr int GR = D / 8;
+  constexpr int NB = D / 32;
+  const int cc = f / NB, nb = f % NB;
+  const int hh = lane >> 5, li = lane & 15;
+  const int d = nb * 32 + ((lane >> 4) & 1) * 16 + 4 * (li & 3);
+  const int r0 = cc * 16 + 4 * hh + (li >> 2);
+  const int r1 = r0 + 8;
+  const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
+  const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// O^T += V^T P^T for one 64-key tile: 16 keys per MFMA, 32 d-rows per MFMA.
+template <int D>
+__device__ __forceinline__ void pv_part(const uint16_t* vs, int lane, const bf16x8 (&pf)[4],
+                                        f32x16 (&oacc)[D / 32]) {
+  constexpr int NB = D / 32;
+  constexpr int NF = 4 * NB;
+  constexpr int PF = kPrefetch > 0 ? kPrefetch : 1;
+  bf16x8 a[PF + 1];
 #pragma unroll
-  for (int cc = 0; cc < 4; ++cc) {
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag<D>(vs, lane, f);
+  sched_fence();
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int d = nb * 32 + dhalf * 16 + dsub;
-      const int r0 = cc * 16 + 4 * hh + rsub;
-      const int r1 = r0 + 8;
-      const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
-      const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
-      typedef short i16x8 __attribute__((ext_vector_type(8)));
-      const i16x8 av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pf[cc], oacc[nb], 0, 0, 0);
-    }
+  for (int f = 0; f < NF; ++f) {
+    const int cc = f / NB, nb = f % NB;
+    oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], pf[cc], oacc[nb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = v_frag<D>(vs, lane, f + PF);
+    sched_fence();
   }
+}
+
+// One 64-key tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
+template <int D>
+__device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t* vs, int lane, int valid,
+                                             const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
+                                             float& lsum, float c) {
+  f32x16 sacc[2];
+  bf16x8 pf[4];
+  s_part<D>(ks, lane, qf, sacc);
+  softmax_part<D>(lane, valid, sacc, pf, oacc, m_used, lsum, c);
+  pv_part<D>(vs, lane, pf, oacc);
 }
 
 // Wait until at most `n` tiles of this wave's DMA loads are still in flight
@@ -298,11 +420,11 @@ __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, in
   wait_tiles_in_flight<kLoads>(rs.issued - 1 - k);
   ring_barrier();
   if (rs.issued < kt_end) {
-    issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<F>(), vbuf<F>());
+    issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<F>(), vbuf<F>());
     ++rs.issued;
     if (rs.issued < kt_end) cursor_next(p, rs.icur);
   }
-  const int valid = tile_valid(p, rs.ccur);
+  const int valid = tile_valid(rs.ccur);
   if (wave_active) tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
   if (k + 1 < kt_end) cursor_next(p, rs.ccur);
 }
@@ -382,16 +504,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   // ---- K/V ring: tile kt lives in stage (kt - kt_begin) % kStages; tiles up
   // to kStages - 1 ahead are in flight while one is computed.
   RingState<D> rs;
-  rs.icur = cursor_at(p, qs, kt_begin);
+  rs.icur = cursor_at(p, qs, kt_begin, b, h);
   rs.ccur = rs.icur;
   rs.issued = kt_begin;
   if (rs.issued < kt_end) {
-    issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<0>(), vbuf<0>());
+    issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<0>(), vbuf<0>());
     if (++rs.issued < kt_end) cursor_next(p, rs.icur);
   }
   if constexpr (kStages > 2) {
     if (rs.issued < kt_end) {
-      issue_tile<D>(p, rs.icur, b, h, wave, voff0, voff1, kbuf<1>(), vbuf<1>());
+      issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<1>(), vbuf<1>());
       if (++rs.issued < kt_end) cursor_next(p, rs.icur);
     }
   }

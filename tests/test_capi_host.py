@@ -127,6 +127,7 @@ def test_argument_errors_launch_nothing():
         assert fn(L, scale=float("nan")) == A
         assert fn(L, ts=2 * 128 - 8) == A              # token stride below H*D
         assert fn(L, ts=2 * 128 + 4) == A              # not a multiple of 8
+        assert fn(L, ts=(1 << 24) + 8) == A            # tile byte offsets would overflow 32 bits
         assert fn(L, lse=FAKE + 2) == A                # misaligned LSE
         assert rc.lib().rc_last_error().decode() != ""
     assert _prefill(L, kc=None) == A
