@@ -119,6 +119,95 @@ def cpu_baseline(wl, mask: str, threads_hint: int):
     }
 
 
+def time_calls(torch, fn, reps=10, warm=2):
+    """Average ms per call of fn() on the current stream (HIP events)."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def extras(torch, rc, wl, gen, dev, static, live, step_ms_main):
+    """Side measurements on the workload's shape:
+    * anchors: prefill and step under the paper's mask and under the isolated
+      cache (anchors detached), with the interaction counts of both; the
+      prefill difference is the anchor overhead of Eq. 4;
+    * one GPU's share of a head-sharded run (3 of 24 heads), automatic splits
+      vs none;
+    * the classifier-free-guidance batch: both branches (B = 2, each with its
+      own anchors and cache) in one step call."""
+    B, H, D = wl.B, wl.H, wl.D
+    out = {}
+    q_s, k_s, v_s = static
+    q_l, k_l, v_l = live
+    anchors = {}
+    for mask in ("paper", "isolated"):
+        Lm = rc.Layout(list(wl.segments), mask)
+        ncm = Lm.rows(rc.ROWS_CACHED)
+        kc = torch.empty((B, H, ncm, D), dtype=torch.bfloat16, device=dev)
+        vc = torch.empty_like(kc)
+        o_s = torch.empty_like(q_s)
+        o_l = torch.empty_like(q_l)
+        pre = time_calls(torch, lambda: rc.ref_kv_prefill(Lm, q_s, k_s, v_s, o=o_s, k_cache=kc, v_cache=vc,
+                                                          scale=wl.scale))
+        sp = Lm.auto_splits(B, H, D)
+        wsb = Lm.workspace_bytes(B, H, D, sp)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+        stp = time_calls(torch, lambda: rc.step_masked_attention(Lm, q_l, k_l, v_l, kc, vc, o=o_l, splits=sp,
+                                                                 workspace=ws if wsb else None, scale=wl.scale))
+        anchors[mask] = {"prefill_ms": pre, "step_ms": stp, "prefill_pairs": Lm.pairs(rc.ENTRY_PREFILL),
+                         "step_pairs": Lm.pairs(rc.ENTRY_STEP)}
+        del kc, vc, o_s, o_l, ws
+    pa, iso = anchors["paper"], anchors["isolated"]
+    anchors["anchor_prefill_overhead_measured"] = pa["prefill_ms"] / iso["prefill_ms"] - 1.0
+    anchors["anchor_prefill_overhead_pairs"] = pa["prefill_pairs"] / iso["prefill_pairs"] - 1.0
+    anchors["anchor_step_overhead_measured"] = pa["step_ms"] / iso["step_ms"] - 1.0
+    anchors["anchor_step_overhead_pairs"] = pa["step_pairs"] / iso["step_pairs"] - 1.0
+    out["anchors_paper_vs_isolated"] = anchors
+
+    L = rc.Layout(list(wl.segments), "perref")
+    n_live, n_cached = L.rows(rc.ROWS_LIVE), L.rows(rc.ROWS_CACHED)
+    flop_pair = 4.0 * D * L.pairs(rc.ENTRY_STEP)
+
+    # one GPU's share of 24 heads over 8 GPUs
+    Hs = max(1, H // 8)
+    ql, kl, vl = (gen_bf16(torch, (B, n_live, Hs, D), gen, wl.std, dev) for _ in range(3))
+    kc, vc = (gen_bf16(torch, (B, Hs, n_cached, D), gen, wl.std, dev) for _ in range(2))
+    o = torch.empty_like(ql)
+    share = {"heads": Hs}
+    for name, sp in (("splits_1", 1), ("splits_auto", 0)):
+        spr = sp if sp else L.auto_splits(B, Hs, D)
+        wsb = L.workspace_bytes(B, Hs, D, spr)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+        ms = time_calls(torch, lambda: rc.step_masked_attention(L, ql, kl, vl, kc, vc, o=o, splits=spr,
+                                                                workspace=ws if wsb else None, scale=wl.scale))
+        share[name] = {"splits": spr, "step_ms": ms, "tflops": flop_pair * B * Hs / (ms * 1e-3) / 1e12}
+    out["one_gpu_head_share"] = share
+    del ql, kl, vl, kc, vc, o
+
+    # classifier-free guidance: both branches in one call
+    Bc = 2
+    ql, kl, vl = (gen_bf16(torch, (Bc, n_live, H, D), gen, wl.std, dev) for _ in range(3))
+    kc, vc = (gen_bf16(torch, (Bc, H, n_cached, D), gen, wl.std, dev) for _ in range(2))
+    o = torch.empty_like(ql)
+    spr = L.auto_splits(Bc, H, D)
+    wsb = L.workspace_bytes(Bc, H, D, spr)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    ms = time_calls(torch, lambda: rc.step_masked_attention(L, ql, kl, vl, kc, vc, o=o, splits=spr,
+                                                            workspace=ws if wsb else None, scale=wl.scale))
+    out["cfg_two_branch_batch"] = {"batch": Bc, "splits": spr, "step_ms": ms,
+                                   "tflops": flop_pair * Bc * H / (ms * 1e-3) / 1e12,
+                                   "vs_two_single_calls": (2 * step_ms_main) / ms}
+    del ql, kl, vl, kc, vc, o, ws
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -129,6 +218,8 @@ def main():
     ap.add_argument("--splits", type=int, default=0, help="split-KV for the step (0 = automatic)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the dense full-recompute comparison")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the side measurements (anchor overhead, one GPU's head share, CFG batch)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (reference for rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -257,6 +348,10 @@ def main():
         }
         del q, k, v, ob
 
+    side = None
+    if not args.no_extras and LAYERS == 1 and B == 1:
+        side = extras(torch, rc, wl, gen, dev, static[0], live[0][0], step_avg)
+
     traffic = measured_traffic(args.config) if splits == 1 else None
     out = {
         "metric": "useful masked-attention TFLOP/s (% of bf16 MFMA peak; per-step ms at 5 refs)",
@@ -299,6 +394,7 @@ def main():
             "useful_flop_per_launch": flop_step,
         },
         "full_recompute": full,
+        "side_measurements": side,
         "paper_context": PAPER_CONTEXT,
         "kernel_source_sha256_16": source_hash(),
         "wall_s_timed": wall,

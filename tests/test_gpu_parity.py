@@ -140,6 +140,21 @@ def test_ref5_headline(preset):
     check_request(workload("ref5"), preset, every=37)
 
 
+def test_ref5_isolated_cache():
+    """The prior-work isolated cache (anchors detached) at the headline shape,
+    the denominator of the anchor-overhead measurement."""
+    check_request(workload("ref5"), "isolated", every=97)
+
+
+def test_ref5_cfg_two_branch_batch():
+    """Classifier-free guidance: both branches in one batch (B = 2), each with
+    its own anchors, references and cache, at the headline shape."""
+    from synthgen import Workload
+    wl = workload("ref5")
+    wl = Workload("ref5_cfg", 2, wl.H, wl.D, wl.segments, std=wl.std, seed=7)
+    check_request(wl, "perref", every=113)
+
+
 def test_ref5_full_recompute_and_step_rows():
     """Full recompute (dense Base over [LT, X, R], and the same cacheable mask)
     on sampled rows; the step's rows equal the same-mask full recompute's
