@@ -163,10 +163,29 @@ def _expect(t, shape, dtype_name, what):
                          f"got {str(t.dtype)} {tuple(t.shape)} contiguous={t.is_contiguous()}")
 
 
-def _stream(stream) -> Optional[int]:
+def _stream(stream, dev) -> Optional[int]:
     torch = _torch()
-    s = torch.cuda.current_stream() if stream is None else stream
+    s = torch.cuda.current_stream(dev) if stream is None else stream
     return s.cuda_stream
+
+
+def _inputs(q, k, v):
+    """Q/K/V: bf16 tensors of one shape on one GPU; returns that device.  The
+    library takes raw device pointers, so a host tensor must never reach it."""
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError(f"q must be a GPU tensor, got device {dev}")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.device != dev or str(t.dtype) != "torch.bfloat16" or tuple(t.shape) != tuple(q.shape):
+            raise ValueError(f"{name} must be a bf16 tensor of shape {tuple(q.shape)} on {dev}, "
+                             f"got {str(t.dtype)} {tuple(t.shape)} on {t.device}")
+    return dev
+
+
+def _same_device(dev, **tensors):
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, the inputs on {dev}")
 
 
 def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_cache=None,
@@ -174,6 +193,7 @@ def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_ca
     """Static-subgraph prefill.  q/k/v: [B, N_static, H, D] bf16 (ST and R
     tokens in sequence order).  Returns (o, lse or None, k_cache, v_cache)."""
     torch = _torch()
+    dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     ts = _tok_stride(q, k, v)
@@ -190,9 +210,11 @@ def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_ca
     _expect(lse, (B, H, N), "torch.float32", "lse")
     _expect(k_cache, (B, H, nc, D), "torch.bfloat16", "k_cache")
     _expect(v_cache, (B, H, nc, D), "torch.bfloat16", "v_cache")
-    _check(lib().rc_ref_kv_prefill(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
-                                   v.data_ptr(), ts, o.data_ptr(), _ptr(lse), k_cache.data_ptr(),
-                                   v_cache.data_ptr(), _stream(stream)))
+    _same_device(dev, o=o, lse=lse, k_cache=k_cache, v_cache=v_cache)
+    with torch.cuda.device(dev):
+        _check(lib().rc_ref_kv_prefill(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                       v.data_ptr(), ts, o.data_ptr(), _ptr(lse), k_cache.data_ptr(),
+                                       v_cache.data_ptr(), _stream(stream, dev)))
     return o, lse, k_cache, v_cache
 
 
@@ -201,6 +223,7 @@ def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse
     """Per-step attention.  q/k/v: [B, N_live, H, D] bf16 (LT and X tokens);
     k_cache/v_cache: [B, H, N_cached, D].  Returns (o, lse or None)."""
     torch = _torch()
+    dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     ts = _tok_stride(q, k, v)
@@ -216,10 +239,12 @@ def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse
     need = layout.workspace_bytes(B, H, D, splits)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    _check(lib().rc_step_masked_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
-                                          v.data_ptr(), ts, _ptr(k_cache), _ptr(v_cache), o.data_ptr(),
-                                          _ptr(lse), splits, _ptr(workspace) if need else None,
-                                          need, _stream(stream)))
+    _same_device(dev, o=o, lse=lse, k_cache=k_cache, v_cache=v_cache, workspace=workspace if need else None)
+    with torch.cuda.device(dev):
+        _check(lib().rc_step_masked_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(),
+                                              k.data_ptr(), v.data_ptr(), ts, _ptr(k_cache), _ptr(v_cache),
+                                              o.data_ptr(), _ptr(lse), splits,
+                                              _ptr(workspace) if need else None, need, _stream(stream, dev)))
     return o, lse
 
 
@@ -227,6 +252,7 @@ def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[fl
                    want_lse: bool = False, stream=None):
     """Full recompute over all rows.  q/k/v: [B, N, H, D] bf16.  Returns (o, lse or None)."""
     torch = _torch()
+    dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     ts = _tok_stride(q, k, v)
@@ -236,6 +262,8 @@ def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[fl
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
     _expect(o, (B, N, H, D), "torch.bfloat16", "o")
     _expect(lse, (B, H, N), "torch.float32", "lse")
-    _check(lib().rc_full_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
-                                   v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _stream(stream)))
+    _same_device(dev, o=o, lse=lse)
+    with torch.cuda.device(dev):
+        _check(lib().rc_full_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                       v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _stream(stream, dev)))
     return o, lse

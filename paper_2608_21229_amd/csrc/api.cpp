@@ -62,13 +62,16 @@ rc_status check_stride(int64_t tok_stride, int32_t H, int32_t D) {
   return RC_OK;
 }
 
-rc_status check_grid(const Params& p) {
-  const int64_t blocks = int64_t(p.B) * p.H * p.n_qtiles * p.splits;
+rc_status check_blocks(int64_t blocks, const char* what) {
   if (blocks >= (int64_t(1) << 31)) {
-    set_error("launch of %lld work-groups exceeds the grid limit", (long long)blocks);
+    set_error("%s launch of %lld work-groups exceeds the grid limit", what, (long long)blocks);
     return RC_ERR_ARG;
   }
   return RC_OK;
+}
+
+rc_status check_grid(const Params& p) {
+  return check_blocks(int64_t(p.B) * p.H * p.n_qtiles * p.splits, "attention");
 }
 
 #define RC_TRY(x)                  \
@@ -162,6 +165,8 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
     }
     c.total_rows = drow;
   }
+  // cache store: one thread per 16-byte granule, 256 per work-group
+  RC_TRY(check_blocks((int64_t(B) * H * n_cached * (D / 8) + 255) / 256, "cache store"));
   RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
   if (n_cached > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
   return RC_OK;
@@ -251,6 +256,8 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
     c.n_rows = int32_t(n_live);
     c.splits = p.splits;
   }
+  // combine: one thread per 4 output elements, 256 per work-group
+  if (p.splits > 1) RC_TRY(check_blocks((int64_t(B) * H * n_live * (D / 4) + 255) / 256, "split-KV combine"));
   RC_TRY(hip_status(launch_attention(p, D, stream), "step attention launch"));
   if (p.splits > 1) RC_TRY(hip_status(launch_combine(c, stream), "split-KV combine launch"));
   return RC_OK;

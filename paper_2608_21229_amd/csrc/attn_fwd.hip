@@ -29,8 +29,7 @@
 // 128-bit K reads and the transpose V reads free of bank conflicts.  The
 // tile cursor keeps the current key range's pointers in scalar registers, so
 // issuing a tile needs no reads of the range table; the K and V fragment
-// reads are software-pipelined kPrefetch MFMAs ahead of their use, and the
-// softmax row max and row sum run as four independent chains.
+// reads are software-pipelined kPrefetch MFMAs ahead of their use.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -106,6 +105,14 @@ __device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int
   c.b = b;
   c.h = h;
   c.r_end = qs.r0 + qs.nr;
+  if (qs.nr == 0) {  // a query segment that reads no key: no tile, and no range entry to read
+    c.k = c.v = nullptr;
+    c.step = 0;
+    c.st = c.rem = c.src = 0;
+    c.r = qs.r0;
+    c.t = c.ntiles = 0;
+    return c;
+  }
   int r = qs.r0;
   for (int i = 0; i + 1 < qs.nr; ++i) {
     const int n = p.range[r].ntiles;
@@ -217,19 +224,11 @@ __device__ __forceinline__ void issue_tile(const Cursor& c, int wave, const uint
 
 __device__ __forceinline__ int tile_valid(const Cursor& c) { return min(kBN, c.rem); }
 
-#ifndef RC_PREFETCH
-#define RC_PREFETCH 3  // LDS fragment reads kept in flight ahead of the MFMA that uses them
-#endif
-constexpr int kPrefetch = RC_PREFETCH;
-#ifndef RC_ILP
-#define RC_ILP 1  // split the softmax max and sum into independent chains
-#endif
+constexpr int kPrefetch = 3;  // LDS fragment reads kept in flight ahead of the MFMA that uses them
 
 // Scheduling fence: the compiler moves no instruction across it, so the
 // software-pipelined order below (reads issued kPrefetch MFMAs ahead) stays.
-__device__ __forceinline__ void sched_fence() {
-  if constexpr (kPrefetch > 0) __builtin_amdgcn_sched_barrier(0);
-}
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // K fragment f = kb * NDC + dc of S^T = K Q^T: rows kb*32 + lane%32,
 // granule 2 dc + lane/32.
@@ -248,7 +247,7 @@ __device__ __forceinline__ void s_part(const uint16_t* ks, int lane, const bf16x
                                        f32x16 (&sacc)[2]) {
   constexpr int NDC = D / 16;
   constexpr int NF = 2 * NDC;
-  constexpr int PF = kPrefetch > 0 ? kPrefetch : 1;
+  constexpr int PF = kPrefetch;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -283,22 +282,11 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
       for (int r = 0; r < 16; ++r)
         if (kb * 32 + 8 * (r >> 2) + (r & 3) >= lim) sacc[kb][r] = -INFINITY;
   }
-#if RC_ILP
-  // four independent max chains (a single wave has no other wave's work to
-  // hide the latency of one serial chain behind)
-  float mq[4] = {sacc[0][0], sacc[0][1], sacc[0][2], sacc[0][3]};
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = (kb == 0 ? 4 : 0); r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], sacc[kb][r]);
-  const float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
-#else
   float mx = sacc[0][0];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-#endif
   const float mt = max_halves(mx) * c;
   if (__any(mt > m_used + kLazyThreshold)) {
     const float m_new = fmaxf(m_used, mt);
@@ -310,19 +298,6 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
       for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
     m_used = m_new;
   }
-#if RC_ILP
-  // four independent partial sums, added to the running sum once per tile
-  float lq[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
-      lq[r & 3] += e;
-      pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
-    }
-  lsum += (lq[0] + lq[1]) + (lq[2] + lq[3]);
-#else
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -331,7 +306,6 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
       lsum += e;
       pf[kb * 2 + (r >> 3)][r & 7] = (__bf16)e;
     }
-#endif
 }
 
 // V^T fragment f = cc * NB + nb of O^T += V^T P^T: two transpose reads of V
@@ -361,7 +335,7 @@ __device__ __forceinline__ void pv_part(const uint16_t* vs, int lane, const bf16
                                         f32x16 (&oacc)[D / 32]) {
   constexpr int NB = D / 32;
   constexpr int NF = 4 * NB;
-  constexpr int PF = kPrefetch > 0 ? kPrefetch : 1;
+  constexpr int PF = kPrefetch;
   bf16x8 a[PF + 1];
 #pragma unroll
   for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag<D>(vs, lane, f);

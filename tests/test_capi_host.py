@@ -141,6 +141,17 @@ def test_argument_errors_launch_nothing():
     assert _step(L, splits=2, ws=FAKE + 4, wsb=need) == W
     # grid overflow: 65535 x 65535 x tiles work-groups
     assert _full(L, B=65535, H=65535, ts=65535 * 128) == A
+    # the cache store's grid (one thread per 16-byte granule) overflows before
+    # the prefill attention's: 2^28 (b, h) pairs x 2 query tiles, 160 cached rows
+    Lc = rc.Layout([(0, 32), (1, 8), (2, 8), (3, 128)], "perref")
+    assert _prefill(Lc, B=16384, H=16384, ts=16384 * 128) == A
+    assert "cache store" in rc.lib().rc_last_error().decode()
+    # the split-KV combine's grid overflows before the step's: 2^26 (b, h)
+    # pairs x 8 query tiles x 2 splits, 2048 live rows
+    Ls = rc.Layout([(0, 64), (1, 256), (2, 1792), (3, 64)], "perref")
+    need = Ls.workspace_bytes(8192, 8192, 128, 2)
+    assert _step(Ls, B=8192, H=8192, ts=8192 * 128, splits=2, ws=FAKE, wsb=need) == A
+    assert "combine" in rc.lib().rc_last_error().decode()
 
 
 def test_layout_errors():
@@ -198,3 +209,17 @@ def test_auto_splits_and_workspace():
     # few key tiles cap the splits at one per 8 key tiles
     L2 = rc.Layout([(1, 64), (2, 64)], "perref")
     assert L2.auto_splits(1, 1, 128) == 1
+
+
+def test_binding_rejects_host_tensors():
+    """The library takes raw device pointers: the binding refuses host tensors
+    (and mismatched shapes) before any call into it."""
+    import pytest
+    import torch
+    L = rc.Layout([(0, 8), (1, 16), (2, 64), (3, 64)], "perref")
+    q = torch.zeros(1, 72, 2, 64, dtype=torch.bfloat16)
+    for fn in (lambda: rc.ref_kv_prefill(L, q, q, q),
+               lambda: rc.full_attention(L, q, q, q),
+               lambda: rc.step_masked_attention(L, q, q, q, None, None)):
+        with pytest.raises(ValueError, match="GPU tensor"):
+            fn()
