@@ -172,6 +172,23 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
                             const void* q, const void* k, const void* v, int64_t tok_stride,
                             void* o, float* lse, void* stream);
 
+/* Dense bf16 projection of the chained synthetic layer (Sec. 3.1, Eq. 2:
+ * per layer K = h W_K, V = h W_V, and the output projection plus residual
+ * that feeds the next layer):
+ *   out[m, n] = bf16( sum_k a[m, k] * w[n, k]  (+ r[m, n]) )
+ * fp32 accumulation in a fixed order, one RNE rounding.  Each output row
+ * depends only on its own input row: a row's result is the same whatever M
+ * is, so projecting the live rows alone reproduces the rows of a projection of
+ * the whole sequence bit for bit.
+ *   a    [M, K] bf16, row stride lda (elements)      w [N, K] bf16, contiguous
+ *   r    [M, N] bf16, row stride ldr, nullable        out [M, N] bf16, row stride ldo
+ * Requirements: N a multiple of 128, K a multiple of 64, K <= 2^22; lda >= K,
+ * ldr >= N, ldo >= N, all multiples of 8 and <= 2^22; pointers 16-byte
+ * aligned; 0 <= M <= 2^40.  `out` may not overlap `a` or `w` (it may be `r`).  M = 0 is a no-op.
+ * RC_ERR_UNSUPPORTED for N or K off those multiples, RC_ERR_ARG otherwise. */
+rc_status rc_linear(int64_t M, int32_t N, int32_t K, const void* a, int64_t lda, const void* w,
+                    const void* r, int64_t ldr, void* out, int64_t ldo, void* stream);
+
 /* Static description of a status code. */
 const char* rc_status_string(rc_status s);
 

@@ -5,13 +5,16 @@ once-per-request reference K/V prefill, per-step masked attention over fresh
 plus cached K/V, and a full-recompute baseline.
 
 The compute lives in ``librefcache.so`` (hand-written HIP, C ABI declared in
-``include/refcache.h``); ``binding`` is its ctypes wrapper.
+``include/refcache.h``); ``binding`` is its ctypes wrapper and ``chain``
+drives a stack of synthetic layers (projection, attention, projection plus
+residual) through it.
 """
 from .binding import (  # noqa: F401
-    Layout, RcError, lib, ref_kv_prefill, step_masked_attention, full_attention,
+    Layout, RcError, lib, ref_kv_prefill, step_masked_attention, full_attention, linear,
     SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF,
     MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE, MASKS,
     ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL,
     ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL,
     RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP,
 )
+from .chain import Chain  # noqa: F401,E402

@@ -55,6 +55,7 @@ SIGNATURES = {
     "rc_step_masked_attention": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                         _i32, _vp, _sz, _vp]),
     "rc_full_attention": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "rc_linear": (_i32, [_i64, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _vp]),
     "rc_status_string": (ctypes.c_char_p, [_i32]),
     "rc_last_error": (ctypes.c_char_p, []),
 }
@@ -267,3 +268,37 @@ def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[fl
         _check(lib().rc_full_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
                                        v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _stream(stream, dev)))
     return o, lse
+
+
+def _rows_view(t, what):
+    """A [M, n] bf16 GPU view with unit column stride; returns its row stride."""
+    if t.dim() != 2 or str(t.dtype) != "torch.bfloat16" or t.device.type != "cuda":
+        raise ValueError(f"{what} must be a 2-D bf16 GPU tensor, got {str(t.dtype)} {tuple(t.shape)} on {t.device}")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{what} must have unit column stride")
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
+def linear(a, w, residual=None, out=None, stream=None):
+    """out = a @ w.T (+ residual), bf16 in and out, fp32 accumulation.
+    a: [M, K] (any row stride); w: [N, K] contiguous; residual, out: [M, N]
+    (any row stride; out may be residual).  Returns out."""
+    torch = _torch()
+    lda = _rows_view(a, "a")
+    dev = a.device
+    M, K = a.shape
+    if w.dim() != 2 or w.shape[1] != K or not w.is_contiguous() or str(w.dtype) != "torch.bfloat16":
+        raise ValueError(f"w must be a contiguous bf16 [N, {K}] tensor, got {str(w.dtype)} {tuple(w.shape)}")
+    N = w.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    for name, t in (("out", out), ("residual", residual)):
+        if t is not None and tuple(t.shape) != (M, N):
+            raise ValueError(f"{name} must have shape {(M, N)}, got {tuple(t.shape)}")
+    ldo = _rows_view(out, "out")
+    ldr = _rows_view(residual, "residual") if residual is not None else 0
+    _same_device(dev, w=w, out=out, residual=residual)
+    with torch.cuda.device(dev):
+        _check(lib().rc_linear(M, N, K, a.data_ptr(), lda, w.data_ptr(), _ptr(residual), ldr, out.data_ptr(), ldo,
+                               _stream(stream, dev)))
+    return out

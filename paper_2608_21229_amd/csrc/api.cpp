@@ -293,4 +293,41 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   return RC_OK;
 }
 
+rc_status rc_linear(int64_t M, int32_t N, int32_t K, const void* a, int64_t lda, const void* w, const void* r,
+                    int64_t ldr, void* out, int64_t ldo, void* stream) {
+  if (M < 0 || M > (int64_t(1) << 40) || N <= 0 || K <= 0) {
+    set_error("linear: M = %lld, N = %d, K = %d must be in [0, 2^40], > 0, > 0", (long long)M, N, K);
+    return RC_ERR_ARG;
+  }
+  if (N % 128 != 0 || K % 64 != 0 || K > (1 << 22)) {
+    set_error("linear: N = %d must be a multiple of 128 and K = %d a multiple of 64 up to 2^22", N, K);
+    return RC_ERR_UNSUPPORTED;
+  }
+  const auto bad_ld = [](int64_t ld, int64_t lo) { return ld < lo || ld % 8 != 0 || ld > (int64_t(1) << 22); };
+  if (bad_ld(lda, K) || bad_ld(ldo, N) || (r && bad_ld(ldr, N))) {
+    set_error("linear: strides lda = %lld, ldr = %lld, ldo = %lld must be >= K / N, multiples of 8, <= 2^22",
+              (long long)lda, (long long)ldr, (long long)ldo);
+    return RC_ERR_ARG;
+  }
+  if (M == 0) return RC_OK;
+  RC_TRY(check_ptr(a, "a"));
+  RC_TRY(check_ptr(w, "w"));
+  RC_TRY(check_ptr(out, "out"));
+  if (r) RC_TRY(check_ptr(r, "r"));
+  RC_TRY(check_blocks((M + 127) / 128 * (N / 128), "linear"));
+  LinearParams q;
+  q.a = static_cast<const uint16_t*>(a);
+  q.w = static_cast<const uint16_t*>(w);
+  q.r = static_cast<const uint16_t*>(r);
+  q.out = static_cast<uint16_t*>(out);
+  q.M = M;
+  q.N = N;
+  q.K = K;
+  q.lda = lda;
+  q.ldr = r ? ldr : 0;
+  q.ldo = ldo;
+  RC_TRY(hip_status(launch_linear(q, stream), "linear launch"));
+  return RC_OK;
+}
+
 }  // extern "C"

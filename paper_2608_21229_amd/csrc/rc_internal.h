@@ -81,6 +81,17 @@ struct CacheStoreParams {
   CopySeg seg[RC_MAX_SEGMENTS];
 };
 
+// Dense projection out = A W^T (+ R) of the chained synthetic layer.
+struct LinearParams {
+  const uint16_t* a;   // [M, K], row stride lda
+  const uint16_t* w;   // [N, K], contiguous
+  const uint16_t* r;   // [M, N], row stride ldr, or null
+  uint16_t* out;       // [M, N], row stride ldo
+  int64_t M;
+  int32_t N, K;
+  int64_t lda, ldr, ldo;
+};
+
 struct CombineParams {
   const float* ws_o;
   const float* ws_ml;
@@ -108,5 +119,6 @@ void set_error(const char* fmt, ...);
 int launch_attention(const Params& p, int D, void* stream);
 int launch_combine(const CombineParams& c, void* stream);
 int launch_cache_store(const CacheStoreParams& c, void* stream);
+int launch_linear(const LinearParams& q, void* stream);  // linear.hip
 
 }  // namespace rc

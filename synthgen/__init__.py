@@ -10,5 +10,5 @@ bfloat16 (round to nearest even), so every consumer sees the same bf16 bits.
 """
 from .workloads import (  # noqa: F401
     ANCHOR, TEXT, TARGET, REF, KIND_NAMES, Workload, WORKLOADS, workload,
-    derive_seed, bf16_normal, draw_qkv, SCALING_KS,
+    derive_seed, bf16_normal, draw_qkv, SCALING_KS, draw_chain_weights, draw_hidden,
 )

@@ -97,3 +97,33 @@ def draw_qkv(B: int, N: int, H: int, D: int, seed: int, std: float = 1.0,
              layer: int = 0, step: int = 0):
     """Q, K, V as [B, N, H, D] bf16 CPU tensors."""
     return tuple(bf16_normal((B, N, H, D), derive_seed(seed, layer, step, t), std) for t in range(3))
+
+
+# ------------------------------------------------- chained synthetic layers
+# Seed slots of the chained-layer draws (the `tensor` argument of derive_seed);
+# 0..5 are the per-layer Q/K/V draws of the attention-only workloads.
+_SLOT_H_STATIC, _SLOT_H_LIVE, _SLOT_W_QKV, _SLOT_W_O = 6, 7, 8, 9
+
+
+def draw_chain_weights(H: int, D: int, layers: int, seed: int):
+    """Per-layer projection weights of a chained synthetic layer, bf16 CPU:
+    w_qkv [3 H D, H D] (rows: Q heads, then K heads, then V heads) and
+    w_o [H D, H D], each N(0, 1 / (H D)) so that projections of an N(0,1)
+    hidden state have unit variance."""
+    C = H * D
+    std = 1.0 / math.sqrt(C)
+    w_qkv = [bf16_normal((3 * C, C), derive_seed(seed, l, 0, _SLOT_W_QKV), std) for l in range(layers)]
+    w_o = [bf16_normal((C, C), derive_seed(seed, l, 0, _SLOT_W_O), std) for l in range(layers)]
+    return w_qkv, w_o
+
+
+def draw_hidden(wl: Workload, step: int = 0):
+    """Layer-0 hidden states [B, N, H D] bf16 N(0,1): the static rows (ST and
+    R tokens in sequence order, fixed for the request) and the live rows (LT
+    and X tokens, fresh at each denoising step)."""
+    C = wl.H * wl.D
+    ns = sum(n for k, n in wl.segments if k in (ANCHOR, REF))
+    nl = sum(n for k, n in wl.segments if k in (TEXT, TARGET))
+    h_static = bf16_normal((wl.B, ns, C), derive_seed(wl.seed, 0, 0, _SLOT_H_STATIC))
+    h_live = bf16_normal((wl.B, nl, C), derive_seed(wl.seed, 0, step + 1, _SLOT_H_LIVE))
+    return h_static, h_live

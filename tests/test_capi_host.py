@@ -223,3 +223,38 @@ def test_binding_rejects_host_tensors():
                lambda: rc.step_masked_attention(L, q, q, q, None, None)):
         with pytest.raises(ValueError, match="GPU tensor"):
             fn()
+
+
+def _lin(M=300, N=256, K=192, a=FAKE, lda=None, w=FAKE, r=None, ldr=0, out=FAKE, ldo=None):
+    lda = K if lda is None else lda
+    ldo = N if ldo is None else ldo
+    return rc.lib().rc_linear(M, N, K, a, lda, w, r, ldr, out, ldo, None)
+
+
+def test_linear_argument_errors_launch_nothing():
+    A, U = rc.RC_ERR_ARG, rc.RC_ERR_UNSUPPORTED
+    assert _lin(M=-1) == A
+    assert _lin(M=2 ** 40 + 1) == A
+    assert _lin(M=2 ** 40) == A                     # grid of 2^34 work-groups
+    assert _lin(N=0) == A and _lin(K=0) == A
+    assert _lin(N=192) == U and _lin(K=96) == U     # off the 128 / 64 tile multiples
+    assert _lin(K=2 ** 22 + 64, lda=2 ** 22 + 64) == U
+    assert _lin(lda=128) == A                       # lda < K
+    assert _lin(lda=196) == A                       # not a multiple of 8
+    assert _lin(lda=2 ** 22 + 8) == A
+    assert _lin(ldo=248) == A
+    assert _lin(r=FAKE, ldr=128) == A               # ldr < N
+    assert _lin(a=FAKE + 8) == A                    # misaligned
+    assert _lin(r=FAKE + 2, ldr=256) == A
+    assert _lin(w=None) == A and _lin(out=None) == A
+    assert _lin(lda=128) == A
+    assert "linear" in rc.lib().rc_last_error().decode()
+    assert _lin(M=0, a=None, w=None, out=None) == rc.RC_OK   # nothing to do
+
+
+def test_linear_binding_rejects_host_tensors():
+    import torch
+    a = torch.zeros(4, 64, dtype=torch.bfloat16)
+    w = torch.zeros(128, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        rc.linear(a, w)
