@@ -225,7 +225,64 @@ def extras(torch, rc, wl, gen, dev, static, live, step_ms_main):
                                    "tflops": flop_pair * Bc * H / (ms * 1e-3) / 1e12,
                                    "vs_two_single_calls": (2 * step_ms_main) / ms}
     del ql, kl, vl, kc, vc, o, ws
+    out["chained_layers"] = chained_layers(torch, rc, wl, dev)
     return out
+
+
+def chained_layers(torch, rc, wl, dev, layers=4, steps=40):
+    """Synthetic layers (fused QKV projection -> masked attention -> output
+    projection + residual) at the workload's shape: the cached path (static
+    rows once through every layer, then the live rows per step) against the
+    full recompute (every row re-projected and attended per step)."""
+    from synthgen import draw_chain_weights, draw_hidden
+    B, H, D = wl.B, wl.H, wl.D
+    C = H * D
+    w_qkv, w_o = draw_chain_weights(H, D, layers, wl.seed)
+    L = rc.Layout(list(wl.segments), "perref")
+    ch = rc.Chain(L, [w.to(dev) for w in w_qkv], [w.to(dev) for w in w_o], H, D)
+    del w_qkv, w_o
+    h_s, h_l = (t.to(dev) for t in draw_hidden(wl, 0))
+    static_pos, live_pos, pos = [], [], 0
+    for k, n in wl.segments:
+        (static_pos if k in (0, 3) else live_pos).extend(range(pos, pos + n))
+        pos += n
+    h0 = torch.empty((B, pos, C), dtype=torch.bfloat16, device=dev)
+    h0[:, torch.tensor(static_pos, device=dev)] = h_s
+    h0[:, torch.tensor(live_pos, device=dev)] = h_l
+    caches = ch.prefill(h_s)
+    pre = time_calls(torch, lambda: ch.prefill(h_s, caches=caches), reps=3, warm=1)
+    stp = time_calls(torch, lambda: ch.step(h_l, caches), reps=10)
+    full = time_calls(torch, lambda: ch.full(h0), reps=3, warm=1)
+    n_live, n_all = L.rows(rc.ROWS_LIVE), L.rows(rc.ROWS_ALL)
+    # useful FLOPs per layer: projections 2 M C (3C + C), attention 4 D H B pairs
+    step_flop = layers * (8.0 * B * n_live * C * C + 4.0 * D * H * B * L.pairs(rc.ENTRY_STEP))
+    full_flop = layers * (8.0 * B * n_all * C * C + 4.0 * D * H * B * L.pairs(rc.ENTRY_FULL))
+    # projections of one step alone (live rows, then all rows), for the split of the time
+    qkv = torch.empty((B * n_live, 3 * C), dtype=torch.bfloat16, device=dev)
+    hw = torch.empty((B * n_live, C), dtype=torch.bfloat16, device=dev)
+    hl2 = h_l.reshape(B * n_live, C)
+    o = hl2.flip(0).contiguous()   # stands in for the attention output: same shape and distribution
+    lin = time_calls(torch, lambda: [(rc.linear(hl2, ch.w_qkv[l], out=qkv),
+                                      rc.linear(o, ch.w_o[l], residual=hl2, out=hw)) for l in range(layers)])
+    # the paper's Base: dense attention over [LT, X, R] (no anchors), all rows re-projected
+    base_segs = [sg for sg in wl.segments if sg[0] != 0]
+    Lb = rc.Layout(base_segs, "dense")
+    ch_base = rc.Chain(Lb, ch.w_qkv, ch.w_o, H, D)
+    n_st = wl.segments[0][1] if wl.segments[0][0] == 0 else 0   # the workloads put ST first, once
+    hb = h0[:, n_st:]
+    assert hb.shape[1] == Lb.rows(rc.ROWS_ALL)
+    base = time_calls(torch, lambda: ch_base.full(hb), reps=3, warm=1)
+    res = {"layers": layers, "mask": "perref", "hidden": C,
+           "dense_base_ms": base, "speedup_per_step_vs_dense_base": base / stp,
+           f"speedup_request_{steps}_steps_vs_dense_base": steps * base / (pre + steps * stp),
+           "prefill_ms": pre, "step_ms": stp, "full_recompute_ms": full,
+           "step_ms_per_layer": stp / layers, "full_recompute_ms_per_layer": full / layers,
+           "step_projection_ms": lin, "step_projection_share": lin / stp,
+           "step_tflops": step_flop / (stp * 1e-3) / 1e12, "full_recompute_tflops": full_flop / (full * 1e-3) / 1e12,
+           "speedup_per_step": full / stp,
+           f"speedup_request_{steps}_steps": steps * full / (pre + steps * stp)}
+    del ch, ch_base, caches, h_s, h_l, h0, hb, qkv, hw, o
+    return res
 
 
 def main():
