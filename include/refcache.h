@@ -58,6 +58,13 @@ extern "C" {
 
 #define RC_MAX_SEGMENTS 32
 
+/* `splits` value of rc_step_masked_attention for the balanced schedule: one
+ * round of 256 work-groups (one per CU), each taking an equal contiguous share
+ * of all (query tile, key tile) work; query tiles cut between work-groups are
+ * merged from fp32 partials in work-group order.  Needs a workspace of
+ * 2 * 256 * 256 * (D + 2) * 4 bytes whatever the problem size. */
+#define RC_SPLITS_BALANCED (-1)
+
 typedef enum {
   RC_OK = 0,
   RC_ERR_ARG = -1,                 /* null/misaligned pointer, bad size or stride */

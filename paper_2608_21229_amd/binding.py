@@ -15,6 +15,7 @@ import os
 from typing import Iterable, Optional, Sequence, Tuple
 
 RC_MAX_SEGMENTS = 32
+SPLITS_BALANCED = -1   # rc_step_masked_attention: one round of 256 work-groups sharing all key tiles evenly
 RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP = 0, -1, -2, -3, -4, -5
 SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
 MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE = 0, 1, 2, 3
@@ -222,7 +223,8 @@ def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_ca
 def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse=None, splits: int = 0,
                           workspace=None, scale: Optional[float] = None, want_lse: bool = False, stream=None):
     """Per-step attention.  q/k/v: [B, N_live, H, D] bf16 (LT and X tokens);
-    k_cache/v_cache: [B, H, N_cached, D].  Returns (o, lse or None)."""
+    k_cache/v_cache: [B, H, N_cached, D].  splits: 0 automatic, 1 none, > 1
+    split-KV, SPLITS_BALANCED the balanced schedule.  Returns (o, lse or None)."""
     torch = _torch()
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape

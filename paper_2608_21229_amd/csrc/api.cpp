@@ -88,6 +88,10 @@ rc_status hip_status(int err, const char* what) {
   return RC_OK;
 }
 
+size_t balanced_workspace_bytes(int32_t D) {
+  return size_t(2) * kBalancedWGs * kBM * size_t(D + 2) * sizeof(float);
+}
+
 void fill_common(Params& p, int32_t B, int32_t H, float scale) {
   p.B = B;
   p.H = H;
@@ -185,8 +189,9 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
 
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
   if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
-  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < 0) return 0;
+  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsBalanced) return 0;
   if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
+  if (splits == kSplitsBalanced) return balanced_workspace_bytes(D);
   if (splits <= 1) return 0;
   const int64_t n_live = count_rows(L, RowSet::Live);
   return size_t(splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
@@ -200,8 +205,8 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   RC_TRY(check_layout(L, RC_ENTRY_STEP));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
-  if (splits < 0 || splits > kMaxSplits) {
-    set_error("splits = %d must be in [0, %d]", splits, kMaxSplits);
+  if (splits < kSplitsBalanced || splits > kMaxSplits) {
+    set_error("splits = %d must be RC_SPLITS_BALANCED (-1) or in [0, %d]", splits, kMaxSplits);
     return RC_ERR_ARG;
   }
   const int64_t n_live = count_rows(L, RowSet::Live);
@@ -221,7 +226,13 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   fill_common(p, B, H, scale);
   RC_TRY(plan(L, RC_ENTRY_STEP, p));
   p.splits = splits == 0 ? auto_splits(p) : splits;
-  RC_TRY(check_grid(p));
+  const bool balanced = p.splits == kSplitsBalanced;
+  if (balanced) {
+    p.units = int64_t(B) * H * p.units_bh;
+    p.bal_wgs = kBalancedWGs;
+  } else {
+    RC_TRY(check_grid(p));
+  }
   p.q = static_cast<const uint16_t*>(q_live);
   p.q_st = tok_stride;
   p.q_sb = tok_stride * n_live;
@@ -233,6 +244,20 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
                     tok_stride * n_live, D, tok_stride};
   p.src[1] = KeySrc{static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache),
                     int64_t(H) * n_cached * D, n_cached * D, D};
+  if (balanced) {
+    const size_t need = balanced_workspace_bytes(D);
+    if (!workspace || !aligned16(workspace) || ws_bytes < need) {
+      set_error("the balanced schedule needs a 16-byte aligned workspace of %zu bytes (got %zu)", need,
+                workspace ? ws_bytes : size_t(0));
+      return RC_ERR_WORKSPACE;
+    }
+    p.ws_o = static_cast<float*>(workspace);
+    p.ws_ml = p.ws_o + size_t(2) * kBalancedWGs * kBM * D;
+    RC_TRY(check_blocks((int64_t(B) * H * n_live * (D / 4) + 255) / 256, "balanced merge"));
+    RC_TRY(hip_status(launch_attention_balanced(p, D, stream), "step attention launch"));
+    RC_TRY(hip_status(launch_combine_balanced(p, D, stream), "balanced merge launch"));
+    return RC_OK;
+  }
   CombineParams c;
   memset(&c, 0, sizeof c);
   if (p.splits > 1) {

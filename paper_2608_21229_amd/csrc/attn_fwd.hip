@@ -403,38 +403,33 @@ __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, in
   if (k + 1 < kt_end) cursor_next(p, rs.ccur);
 }
 
-template <int D, bool kSplit>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
+// Logical work-group index: the hardware deals blocks round-robin to the 8
+// XCDs; remap so that each XCD receives a contiguous run of logical indices,
+// i.e. neighbouring work items (the query tiles of one head, which stream the
+// same K/V) share one XCD's L2.
+__device__ __forceinline__ int xcd_logical_block(int bid, int nblk) {
+  const int xcd = bid & 7, kx = bid >> 3, per = nblk >> 3, rem = nblk & 7;
+  return (xcd < rem) ? xcd * (per + 1) + kx : rem * (per + 1) + (xcd - rem) * per + kx;
+}
+
+// One query tile t of segment qs, batch b, head h, over the segment's key
+// tiles [kt_begin, kt_end).  part_row < 0: final output (bf16 O and LSE);
+// otherwise unnormalised fp32 partials (O, running max in log2 units, row
+// sum) at workspace row part_row + (row inside the tile).
+template <int D>
+__device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int t, int b, int h, int kt_begin,
+                                            int kt_end, int64_t part_row, int wave, int lane) {
   constexpr int GR = D / 8;
   constexpr int NDC = D / 16;  // 16-wide d chunks of the QK^T contraction
   constexpr int NB = D / 32;   // 32-wide d blocks of the output
   constexpr int kLoads = kBN * GR / kThreads;
   static_assert(kLoads >= 1 && kBN * GR % kThreads == 0, "tile granules must divide over the threads");
   static_assert(kStages >= 2 && kStages <= 3, "stage ring of 2 or 3 tiles");
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5;  // which 32-lane half
 
-  // ---- work item: XCD-aware remap so consecutive logical items (same head)
-  // share one XCD's L2.  The hardware deals blocks to the 8 XCDs round-robin.
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int xcd = bid & 7, kx = bid >> 3, per = nblk >> 3, rem = nblk & 7;
-  const int w = (xcd < rem) ? xcd * (per + 1) + kx : rem * (per + 1) + (xcd - rem) * per + kx;
-  const int split = w % p.splits;
-  int rest = w / p.splits;
-  const int t = rest % p.n_qtiles;
-  rest /= p.n_qtiles;
-  const int h = rest % p.H, b = rest / p.H;
-
-  int qi = 0;
-  while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
-  const QSeg qs = p.qseg[qi];
   const int seg_row0 = (t - qs.tile0) * kBM;
   const int rows_valid = min(kBM, qs.len - seg_row0);
   const int row0 = qs.row0 + seg_row0;  // first row of the tile in the Q/O buffers
-  const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
-  const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
   const bool wave_active = wave * 32 < rows_valid;  // wave-uniform
 
   // per-lane byte offsets of this lane's granules inside a tile, per key source
@@ -505,9 +500,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   // ---- epilogue
   const float l_tot = sum_halves(lsum);
   if (!row_ok) return;
-  const int grow = row0 + my_row;
-  if constexpr (kSplit) {
-    const int64_t prow = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + grow;
+  if (part_row >= 0) {
+    const int64_t prow = part_row + my_row;
     float* op = p.ws_o + prow * D;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
@@ -522,6 +516,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
       p.ws_ml[prow * 2 + 1] = l_tot;
     }
   } else {
+    const int grow = row0 + my_row;
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(grow) * p.o_st + int64_t(h) * D;
 #pragma unroll
@@ -539,6 +534,124 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
           l_tot > 0.f ? m_used * 0.69314718055994531f + __logf(l_tot) : -INFINITY;
   }
 }
+
+// One work-group per (batch, head, query tile, key split).
+template <int D, bool kSplit>
+__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int w = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int split = w % p.splits;
+  int rest = w / p.splits;
+  const int t = rest % p.n_qtiles;
+  rest /= p.n_qtiles;
+  const int h = rest % p.H, b = rest / p.H;
+
+  int qi = 0;
+  while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
+  const QSeg qs = p.qseg[qi];
+  const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
+  const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+  int64_t part_row = -1;
+  if constexpr (kSplit)
+    part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * kBM;
+  attend_tile<D>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
+}
+
+// Balanced schedule: work-group g of G takes the key-tile units
+// [g W / G, (g + 1) W / G) of the W units, ordered by (batch, head, query
+// segment, query tile, key tile).  A query tile wholly inside one range is
+// written directly; a cut one leaves partials: the work-group's first piece
+// in workspace slot 2 g, its last piece (when not also its first) in 2 g + 1.
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_fwd_balanced_kernel(const Params p) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int64_t G = gridDim.x;
+  int64_t u = int64_t(g) * p.units / G;
+  const int64_t hi = int64_t(g + 1) * p.units / G;
+  bool first = true;
+  while (u < hi) {
+    const int64_t bh = u / p.units_bh;
+    int64_t r = u - bh * p.units_bh;
+    int qi = 0;
+    while (qi + 1 < p.n_qseg && p.qseg[qi + 1].unit0 <= r) ++qi;
+    const QSeg qs = p.qseg[qi];
+    r -= qs.unit0;
+    const int tl = int(r / qs.ktiles);
+    const int kt0 = int(r - int64_t(tl) * qs.ktiles);
+    const int kt1 = int(min(int64_t(qs.ktiles), int64_t(kt0) + (hi - u)));
+    const bool whole = kt0 == 0 && kt1 == qs.ktiles;
+    const int64_t part_row = whole ? -1 : int64_t(first ? 2 * g : 2 * g + 1) * kBM;
+    if (!first) ring_barrier();  // every wave is done with the previous piece's LDS stages
+    attend_tile<D>(p, qs, qs.tile0 + tl, int(bh / p.H), int(bh % p.H), kt0, kt1, part_row, wave, lane);
+    u += kt1 - kt0;
+    first = false;
+  }
+}
+
+// Merge of the balanced schedule, one thread per (row, 4 consecutive d):
+// rows of a query tile that lies inside one work-group's range were written by
+// the attention kernel and are skipped; a cut tile merges the partials of the
+// work-groups g_first .. g_last that cover it, in that order (the key order);
+// rows that read no key get O = 0 and LSE = -inf.
+__global__ __launch_bounds__(256) void combine_balanced_kernel(const Params p, int D) {
+  const int dq = D / 4;
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t total = int64_t(p.B) * p.H * p.n_rows * dq;
+  if (idx >= total) return;
+  const int d4 = int(idx % dq);
+  const int64_t bhr = idx / dq;  // (b*H + h)*n_rows + row
+  const int row = int(bhr % p.n_rows);
+  const int64_t bh = bhr / p.n_rows;
+  const int h = int(bh % p.H), b = int(bh / p.H);
+  int qi = 0;
+  while (qi + 1 < p.n_qseg && p.qseg[qi + 1].row0 <= row) ++qi;
+  const QSeg& qs = p.qseg[qi];
+  const int tl = (row - qs.row0) / kBM, rin = (row - qs.row0) % kBM;
+  uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(row) * p.o_st + int64_t(h) * D + 4 * d4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float M = -INFINITY, l = 0.f;
+  if (qs.ktiles > 0) {
+    const int64_t W = p.units, G = p.bal_wgs;
+    const int64_t s = bh * p.units_bh + qs.unit0 + int64_t(tl) * qs.ktiles;
+    const int64_t e = s + qs.ktiles;
+    // work-group holding unit x: the largest g with floor(g W / G) <= x
+    const int64_t gf = ((s + 1) * G - 1) / W, gl = (e * G - 1) / W;
+    if (gf == gl) return;
+    // work-groups with an empty range (more work-groups than units) write nothing
+    for (int64_t g = gf; g <= gl; ++g) {
+      const int64_t lo = g * W / G;
+      if (lo == (g + 1) * W / G) continue;
+      const int64_t slot = (g == gf && lo < s) ? 2 * g + 1 : 2 * g;
+      const int64_t prow = slot * kBM + rin;
+      if (p.ws_ml[prow * 2 + 1] > 0.f) M = fmaxf(M, p.ws_ml[prow * 2]);
+    }
+    if (M != -INFINITY) {
+      for (int64_t g = gf; g <= gl; ++g) {
+        const int64_t lo = g * W / G;
+        if (lo == (g + 1) * W / G) continue;
+        const int64_t slot = (g == gf && lo < s) ? 2 * g + 1 : 2 * g;
+        const int64_t prow = slot * kBM + rin;
+        const float ls = p.ws_ml[prow * 2 + 1];
+        if (!(ls > 0.f)) continue;
+        const float wgt = __builtin_amdgcn_exp2f(p.ws_ml[prow * 2] - M);
+        const float4 o = *reinterpret_cast<const float4*>(p.ws_o + prow * D + 4 * d4);
+        acc.x += wgt * o.x;
+        acc.y += wgt * o.y;
+        acc.z += wgt * o.z;
+        acc.w += wgt * o.w;
+        l += wgt * ls;
+      }
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  __bf16 o4[4] = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv), (__bf16)(acc.w * inv)};
+  *reinterpret_cast<u32x2*>(op) = __builtin_bit_cast(u32x2, o4);
+  if (p.lse && d4 == 0) p.lse[bhr] = l > 0.f ? M * 0.69314718055994531f + __logf(l) : -INFINITY;
+}
+
 
 // Split-KV merge: O = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s, in split order.
 // One thread per (row, 4 consecutive d).
@@ -615,6 +728,22 @@ int launch_attention(const Params& p, int D, void* stream) {
     if (split) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, s, p);
     else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, p);
   }
+  return int(hipGetLastError());
+}
+
+int launch_attention_balanced(const Params& p, int D, void* stream) {
+  if (p.units == 0) return 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (D == 128) hipLaunchKernelGGL(attn_fwd_balanced_kernel<128>, dim3(p.bal_wgs), dim3(kThreads), 0, s, p);
+  else hipLaunchKernelGGL(attn_fwd_balanced_kernel<64>, dim3(p.bal_wgs), dim3(kThreads), 0, s, p);
+  return int(hipGetLastError());
+}
+
+int launch_combine_balanced(const Params& p, int D, void* stream) {
+  const int64_t total = int64_t(p.B) * p.H * p.n_rows * (D / 4);
+  if (total == 0) return 0;
+  hipLaunchKernelGGL(combine_balanced_kernel, dim3((total + 255) / 256), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), p, D);
   return int(hipGetLastError());
 }
 

@@ -150,6 +150,7 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
   p.n_rows = pos_rows;
   p.n_qseg = 0;
   p.n_qtiles = 0;
+  p.units_bh = 0;
   int nranges = 0;
   for (int q = 0; q < L->n_seg; ++q) {
     if (row_of[q] < 0) continue;
@@ -203,7 +204,10 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
     s.r0 = r0;
     s.nr = nr;
     s.ktiles = ktiles;
-    p.n_qtiles += (s.len + kBM - 1) / kBM;
+    s.unit0 = p.units_bh;
+    const int ntiles = (s.len + kBM - 1) / kBM;
+    p.n_qtiles += ntiles;
+    p.units_bh += int64_t(ntiles) * ktiles;
   }
   return RC_OK;
 }

@@ -28,6 +28,10 @@ constexpr int kBM = 32 * kWaves;  // query rows per work-group
 constexpr int kBN = 64;           // keys per K/V tile
 constexpr int kMaxRanges = 96;    // merged key ranges over all query segments
 constexpr int kMaxSplits = 32;
+// Balanced step schedule: one round of work-groups (one per CU of the 256),
+// each taking an equal contiguous share of all (query tile, key tile) units.
+constexpr int kBalancedWGs = 256;
+constexpr int32_t kSplitsBalanced = RC_SPLITS_BALANCED;
 
 struct KeyRange {
   int32_t start;   // first key token inside its source
@@ -37,6 +41,7 @@ struct KeyRange {
 };
 
 struct QSeg {
+  int64_t unit0;   // key-tile units of the earlier query segments, per (batch, head)
   int32_t row0;    // first row inside the Q/O buffers
   int32_t len;     // rows
   int32_t tile0;   // index of this segment's first query tile
@@ -60,7 +65,10 @@ struct Params {
   float* ws_o;         // split partials [splits, B, H, n_rows, D] (unnormalised)
   float* ws_ml;        // split partials [splits, B, H, n_rows, 2] (max in log2 units, sum)
   KeySrc src[2];
-  int32_t B, H, n_rows, n_qseg, n_qtiles, splits;
+  int32_t B, H, n_rows, n_qseg, n_qtiles, splits;  // splits: kSplitsBalanced = balanced schedule
+  int64_t units_bh;    // key-tile units (query tile x key tile) per (batch, head)
+  int64_t units;       // B * H * units_bh
+  int32_t bal_wgs;     // work-groups of the balanced schedule
   float scale_log2;    // softmax scale * log2(e)
   QSeg qseg[RC_MAX_SEGMENTS];
   KeyRange range[kMaxRanges];
@@ -118,6 +126,8 @@ void set_error(const char* fmt, ...);
 // Kernel launchers (attn_fwd.hip).  Return a hipError_t as int.
 int launch_attention(const Params& p, int D, void* stream);
 int launch_combine(const CombineParams& c, void* stream);
+int launch_attention_balanced(const Params& p, int D, void* stream);
+int launch_combine_balanced(const Params& p, int D, void* stream);
 int launch_cache_store(const CacheStoreParams& c, void* stream);
 int launch_linear(const LinearParams& q, void* stream);  // linear.hip
 

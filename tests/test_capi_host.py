@@ -132,8 +132,13 @@ def test_argument_errors_launch_nothing():
         assert rc.lib().rc_last_error().decode() != ""
     assert _prefill(L, kc=None) == A
     assert _step(L, vc=None) == A
-    assert _step(L, splits=-1) == A
+    assert _step(L, splits=-2) == A
     assert _step(L, splits=33) == A
+    assert _step(L, splits=-1) == W                    # balanced schedule, no workspace
+    need_bal = L.workspace_bytes(1, 2, 128, -1)
+    assert need_bal == 2 * 256 * 256 * 130 * 4         # fixed: two partial tiles per work-group
+    assert L.workspace_bytes(1, 2, 64, -1) == 2 * 256 * 256 * 66 * 4
+    assert _step(L, splits=-1, ws=FAKE, wsb=need_bal - 1) == W
     assert _step(L, splits=2) == W                     # no workspace
     need = L.workspace_bytes(1, 2, 128, 2)
     assert need == 2 * 1 * 2 * 80 * 130 * 4
@@ -152,6 +157,9 @@ def test_argument_errors_launch_nothing():
     need = Ls.workspace_bytes(8192, 8192, 128, 2)
     assert _step(Ls, B=8192, H=8192, ts=8192 * 128, splits=2, ws=FAKE, wsb=need) == A
     assert "combine" in rc.lib().rc_last_error().decode()
+    need = Ls.workspace_bytes(8192, 8192, 128, -1)
+    assert _step(Ls, B=8192, H=8192, ts=8192 * 128, splits=-1, ws=FAKE, wsb=need) == A
+    assert "balanced merge" in rc.lib().rc_last_error().decode()
 
 
 def test_layout_errors():

@@ -103,7 +103,7 @@ RAGGED = [
 def test_ragged_segments(name, segs, preset, D):
     from synthgen import Workload
     wl = Workload(f"{name}_D{D}", 2, 3, D, tuple(segs), std=1.0, seed=11)
-    for splits in (1, 3, 0):
+    for splits in (1, 3, 0, rc.SPLITS_BALANCED):
         check_request(wl, preset, splits=splits)
 
 
@@ -195,7 +195,7 @@ def test_mixed48_layers(layer):
     check_request(workload("mixed48"), "perref", every=53, layer=layer, steps=(0, 39))
 
 
-@pytest.mark.parametrize("splits", [1, 2, 4, 7, 0])
+@pytest.mark.parametrize("splits", [1, 2, 4, 7, 0, -1])
 def test_split_kv_one_gpu_share(splits):
     """Headline shape at one GPU's share of heads (3 of 24): few query tiles,
     so split-KV carries the occupancy."""
@@ -229,7 +229,7 @@ def test_determinism_and_nan_poison():
     kc_c, vc_c = kc, vc
     ql, kl, vl = (t.to(DEV) for t in inp.live)
     runs = []
-    for splits in (1, 1, 3, 3):
+    for splits in (1, 1, 3, 3, -1, -1):
         ol = torch.full_like(ql, float("nan"))
         lse = torch.full((B, H, ql.shape[1]), float("nan"), device=DEV)
         rc.step_masked_attention(L, ql, kl, vl, kc_c, vc_c, o=ol, lse=lse, splits=splits, scale=wl.scale)
@@ -239,6 +239,7 @@ def test_determinism_and_nan_poison():
         assert not torch.isnan(ol).any() and not torch.isnan(lse).any()
     assert torch.equal(runs[0][0], runs[1][0]) and torch.equal(runs[0][1], runs[1][1])
     assert torch.equal(runs[2][0], runs[3][0]) and torch.equal(runs[2][1], runs[3][1])
+    assert torch.equal(runs[4][0], runs[5][0]) and torch.equal(runs[4][1], runs[5][1])
 
 
 def test_fused_qkv_views_and_batch():
@@ -263,3 +264,48 @@ def test_fused_qkv_views_and_batch():
     Ol, lsl, _ = oracle_step(inp, vis, kcr, vcr, wl.scale)
     check(ol, Ol, "fused step")
     check_lse(lsel, lsl, "fused step")
+
+
+@pytest.mark.parametrize("preset", ["perref", "paper", "isolated"])
+def test_tiny_balanced_schedule(preset):
+    """Balanced schedule on the tiny workload: 16 key-tile units over 256
+    work-groups, so every query tile is cut into one-tile pieces and merged."""
+    check_request(workload("tiny"), preset, splits=rc.SPLITS_BALANCED, steps=(0, 1))
+
+
+def test_ref5_balanced_schedule():
+    """Headline shape under the balanced schedule (432 query tiles of 393 key
+    tiles dealt over 256 work-groups), sampled rows, two steps."""
+    check_request(workload("ref5"), "perref", every=89, splits=rc.SPLITS_BALANCED, steps=(0, 1))
+
+
+def test_ref5_cfg_batch_balanced():
+    from synthgen import Workload
+    wl = workload("ref5")
+    wl = Workload("ref5_cfg_bal", 2, wl.H, wl.D, wl.segments, seed=9)
+    check_request(wl, "perref", every=131, splits=rc.SPLITS_BALANCED)
+
+
+@pytest.mark.parametrize("splits", [1, 3, -1])
+def test_step_query_segment_without_keys(splits):
+    """A live segment that reads no key: O = 0 and LSE = -inf on its rows
+    (written by the merge under the balanced schedule), next to segments that
+    read many."""
+    from synthgen import Workload
+    segs = ((0, 40), (1, 300), (2, 520), (3, 200), (3, 77))
+    wl = Workload("nokeys", 2, 2, 128, segs, seed=13)
+    n = len(segs)
+    vis = om.perref_mask(wl.kinds)
+    vis = [list(r) for r in vis]
+    vis[1] = [False] * n          # LT reads nothing
+    inp = draw_inputs(wl)
+    L = rc.Layout(list(segs), vis)
+    scale = wl.scale
+    o, lse, kc, vc = run_prefill(L, inp, scale)
+    ol, lsel = run_step(L, inp, kc, vc, scale, splits=splits)
+    torch.cuda.synchronize()
+    _, _, _, Kc, Vc = oracle_prefill(inp, vis, scale)
+    Ol, Ll, _ = oracle_step(inp, vis, Kc, Vc, scale)
+    check(ol, Ol, f"no-key segment step splits={splits} O")
+    check_lse(lsel, Ll, f"no-key segment step splits={splits}")
+    assert bool((ol[:, :300] == 0).all()) and bool(torch.isinf(lsel[:, :, :300]).all())
