@@ -226,7 +226,43 @@ def extras(torch, rc, wl, gen, dev, static, live, step_ms_main):
                                    "vs_two_single_calls": (2 * step_ms_main) / ms}
     del ql, kl, vl, kc, vc, o, ws
     out["chained_layers"] = chained_layers(torch, rc, wl, dev)
+    out["fp8_cache"] = fp8_cache(torch, rc, wl, dev, static, live, step_ms_main)
     return out
+
+
+def fp8_cache(torch, rc, wl, dev, static, live, step_ms_main):
+    """The FP8 (e4m3) reference cache at the workload's shape: prefill and step
+    times, cache bytes per layer, and the output's relative L2 distance from the
+    bf16 cache's (the approximation the 8-bit cache makes)."""
+    B, H, D = wl.B, wl.H, wl.D
+    L = rc.Layout(list(wl.segments), "perref")
+    q_s, k_s, v_s = static
+    q_l, k_l, v_l = live
+    o_s = torch.empty_like(q_s)
+    o8 = torch.empty_like(q_l)
+    ob = torch.empty_like(q_l)
+    _, _, kc, vc = rc.ref_kv_prefill(L, q_s, k_s, v_s, scale=wl.scale)
+    _, _, k8, v8t, sc = rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, scale=wl.scale)
+    sp = L.auto_splits(B, H, D)
+    wsb = L.workspace_bytes(B, H, D, sp)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    pre = time_calls(torch, lambda: rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, o=o_s, k_cache8=k8, v_cache8t=v8t,
+                                                          kv_scale=sc, scale=wl.scale), reps=5)
+    stp = time_calls(torch, lambda: rc.step_masked_attention_fp8(L, q_l, k_l, v_l, k8, v8t, sc, o=o8, splits=sp,
+                                                                 workspace=ws if wsb else None, scale=wl.scale))
+    rc.step_masked_attention(L, q_l, k_l, v_l, kc, vc, o=ob, splits=sp, workspace=ws if wsb else None,
+                             scale=wl.scale)
+    torch.cuda.synchronize()
+    rel = ((o8.float() - ob.float()).norm() / ob.float().norm()).item()
+    flop = 4.0 * D * H * B * L.pairs(rc.ENTRY_STEP)
+    res = {"format": "e4m3fn codes, one power-of-two scale per (batch, head) for K and for V",
+           "prefill_ms": pre, "step_ms": stp, "step_tflops": flop / (stp * 1e-3) / 1e12,
+           "step_vs_bf16_cache": step_ms_main / stp,
+           "cache_bytes_per_layer": int(k8.numel() + v8t.numel() + 4 * sc.numel()),
+           "bf16_cache_bytes_per_layer": int(2 * (kc.numel() + vc.numel())),
+           "output_rel_l2_vs_bf16_cache": rel}
+    del kc, vc, k8, v8t, sc, o_s, o8, ob, ws
+    return res
 
 
 def chained_layers(torch, rc, wl, dev, layers=4, steps=40):

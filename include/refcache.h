@@ -101,7 +101,9 @@ typedef enum {
   RC_ROWS_STATIC = 0,  /* tokens of ST and R segments */
   RC_ROWS_LIVE = 1,    /* tokens of LT and X segments */
   RC_ROWS_CACHED = 2,  /* tokens of the cached segments */
-  RC_ROWS_ALL = 3      /* all tokens */
+  RC_ROWS_ALL = 3,     /* all tokens */
+  RC_ROWS_CACHED_FP8 = 4  /* key positions of the FP8 cache: each cached segment starts at a
+                             multiple of 16, the total rounded up to 16 (N_pad) */
 } rc_rows_kind;
 
 typedef struct {
@@ -178,6 +180,35 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
 rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                             const void* q, const void* k, const void* v, int64_t tok_stride,
                             void* o, float* lse, void* stream);
+
+/* FP8 reference cache (the paper calls caching complementary to other
+ * accelerations, Sec. 1 and Sec. 4.2; storing the cache in e4m3 halves its bytes,
+ * its residency and the step's cached-key traffic).
+ *   k_cache8   [B, H, N_pad, D] e4m3fn codes (bytes), rows in the cache order of
+ *              the bf16 cache but each cached segment starting at a multiple of
+ *              16 (RC_ROWS_CACHED_FP8 gives N_pad); padding rows hold zeros.
+ *   v_cache8t  [B, H, D, N_pad] e4m3fn codes: V transposed (d-major), same key
+ *              positions and zero padding.
+ *   kv_scale   [B, H, 2] fp32: the scales s_K, s_V of each (batch, head).
+ * Quantisation, per (b, h) and tensor X in {K, V} over the cached rows:
+ *   amax = max |x|;  s = 2^e with e the smallest integer such that amax / s <= 448
+ *   (s = 1 when amax = 0);  code = e4m3fn(x / s), round to nearest even (x / s is
+ *   exact);  the step reads code * s, exact in bf16.
+ * rc_ref_kv_prefill_fp8 computes the same static-row attention as
+ * rc_ref_kv_prefill (o_static, lse_static) and writes the FP8 cache instead of the
+ * bf16 one.  rc_step_masked_attention_fp8 is rc_step_masked_attention with the
+ * cached K/V read from the FP8 cache (fresh LT/X K/V stay bf16); splits and
+ * workspace as there.  Cache pointers 16-byte aligned; kv_scale 4-byte aligned
+ * (written by the prefill, read by the step).  Errors as the bf16 entries. */
+rc_status rc_ref_kv_prefill_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                const void* q_static, const void* k_static, const void* v_static,
+                                int64_t tok_stride, void* o_static, float* lse_static, void* k_cache8,
+                                void* v_cache8t, float* kv_scale, void* stream);
+rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                       const void* q_live, const void* k_live, const void* v_live,
+                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8t,
+                                       const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
+                                       void* workspace, size_t ws_bytes, void* stream);
 
 /* Dense bf16 projection of the chained synthetic layer (Sec. 3.1, Eq. 2:
  * per layer K = h W_K, V = h W_V, and the output projection plus residual

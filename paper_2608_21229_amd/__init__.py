@@ -11,10 +11,11 @@ residual) through it.
 """
 from .binding import (  # noqa: F401
     Layout, RcError, lib, ref_kv_prefill, step_masked_attention, full_attention, linear,
+    ref_kv_prefill_fp8, step_masked_attention_fp8, fp8_cache_shapes,
     SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF,
     MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE, MASKS,
     ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL,
-    ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL, SPLITS_BALANCED,
+    ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL, ROWS_CACHED_FP8, SPLITS_BALANCED,
     RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP,
 )
 from .chain import Chain  # noqa: F401,E402

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librefcache.so")
-SOURCES = ["layout.cpp", "api.cpp", "attn_fwd.hip", "linear.hip"]
+SOURCES = ["layout.cpp", "api.cpp", "attn_fwd.hip", "linear.hip", "fp8_cache.hip"]
 ARCH = "gfx950"
 
 

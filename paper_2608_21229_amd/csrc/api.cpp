@@ -92,6 +92,12 @@ size_t balanced_workspace_bytes(int32_t D) {
   return size_t(2) * kBalancedWGs * kBM * size_t(D + 2) * sizeof(float);
 }
 
+// A bf16 key source from element strides (batch, head, token) shared by K and V.
+KeySrc bf16_source(const void* k, const void* v, int64_t sb, int64_t sh, int64_t st) {
+  return KeySrc{static_cast<const char*>(k), static_cast<const char*>(v), 2 * sb, 2 * sh, 2 * st, 2 * sb, 2 * sh,
+                2 * st, 0};
+}
+
 void fill_common(Params& p, int32_t B, int32_t H, float scale) {
   p.B = B;
   p.H = H;
@@ -100,25 +106,26 @@ void fill_common(Params& p, int32_t B, int32_t H, float scale) {
   p.lse = nullptr;
   p.ws_o = nullptr;
   p.ws_ml = nullptr;
-  p.src[1] = KeySrc{nullptr, nullptr, 0, 0, 0};
+  p.src[1] = KeySrc{nullptr, nullptr, 0, 0, 0, 0, 0, 0, 0};
 }
 
 }  // namespace
 }  // namespace rc
 
-using namespace rc;
+namespace rc {
+namespace {
 
-extern "C" {
-
-rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
-                            const void* q_static, const void* k_static, const void* v_static,
-                            int64_t tok_stride, void* o_static, float* lse_static, void* k_cache,
-                            void* v_cache, void* stream) {
+// The prefill of both cache formats: static-row attention, then the bf16 cache
+// store or the FP8 quantising store.
+rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q_static,
+                       const void* k_static, const void* v_static, int64_t tok_stride, void* o_static,
+                       float* lse_static, bool fp8, void* k_cache, void* v_cache, float* kv_scale, void* stream) {
   RC_TRY(check_layout(L, RC_ENTRY_PREFILL));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
   const int64_t n_static = count_rows(L, RowSet::Static);
   const int64_t n_cached = count_cached_rows(L);
+  const int64_t n_pad = count_cached_rows_aligned(L, kFp8Align);
   if (n_static == 0) return RC_OK;  // no ST/R segment: nothing to prefill
   RC_TRY(check_ptr(q_static, "q_static"));
   RC_TRY(check_ptr(k_static, "k_static"));
@@ -126,8 +133,17 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   RC_TRY(check_ptr(o_static, "o_static"));
   RC_TRY(check_lse(lse_static, "lse_static"));
   if (n_cached > 0) {
-    RC_TRY(check_ptr(k_cache, "k_cache"));
-    RC_TRY(check_ptr(v_cache, "v_cache"));
+    RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
+    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8t" : "v_cache"));
+    if (fp8) RC_TRY(check_lse(kv_scale, "kv_scale"));
+    if (fp8 && !kv_scale) {
+      set_error("kv_scale is null");
+      return RC_ERR_ARG;
+    }
+    if (fp8 && n_pad > (int64_t(1) << 22)) {
+      set_error("FP8 cache of %lld keys per (batch, head) exceeds 2^22", (long long)n_pad);
+      return RC_ERR_ARG;
+    }
   }
   Params p;
   memset(&p, 0, sizeof p);
@@ -141,67 +157,79 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   p.o_st = int64_t(H) * D;
   p.o_sb = p.o_st * n_static;
   p.lse = lse_static;
-  p.src[0] = KeySrc{static_cast<const uint16_t*>(k_static), static_cast<const uint16_t*>(v_static),
-                    tok_stride * n_static, D, tok_stride};
+  p.src[0] = bf16_source(k_static, v_static, tok_stride * n_static, D, tok_stride);
 
-  CacheStoreParams c;
-  memset(&c, 0, sizeof c);
-  if (n_cached > 0) {
-    c.k_src = static_cast<const uint16_t*>(k_static);
-    c.v_src = static_cast<const uint16_t*>(v_static);
-    c.k_dst = static_cast<uint16_t*>(k_cache);
-    c.v_dst = static_cast<uint16_t*>(v_cache);
-    c.src_st = tok_stride;
-    c.src_sb = tok_stride * n_static;
-    c.B = B;
-    c.H = H;
-    c.D = D;
-    c.n_cached = int32_t(n_cached);
+  // the cached segments' rows inside the static buffers and their cache
+  // positions (padded to multiples of kFp8Align in the FP8 cache)
+  CopySeg seg[RC_MAX_SEGMENTS];
+  int n_copy = 0;
+  {
     const uint32_t cm = cached_mask(L);
     int32_t srow = 0, drow = 0;
     for (int i = 0; i < L->n_seg; ++i) {
       if (!is_static_kind(L->seg[i].kind)) continue;
       if (cm >> i & 1u) {
-        c.seg[c.n_copy++] = CopySeg{srow, L->seg[i].len, drow};
+        if (fp8) drow = (drow + kFp8Align - 1) / kFp8Align * kFp8Align;
+        seg[n_copy++] = CopySeg{srow, L->seg[i].len, drow};
         drow += L->seg[i].len;
       }
       srow += L->seg[i].len;
     }
-    c.total_rows = drow;
   }
-  // cache store: one thread per 16-byte granule, 256 per work-group
-  RC_TRY(check_blocks((int64_t(B) * H * n_cached * (D / 8) + 255) / 256, "cache store"));
+  if (!fp8) {
+    CacheStoreParams c;
+    memset(&c, 0, sizeof c);
+    if (n_cached > 0) {
+      c.k_src = static_cast<const uint16_t*>(k_static);
+      c.v_src = static_cast<const uint16_t*>(v_static);
+      c.k_dst = static_cast<uint16_t*>(k_cache);
+      c.v_dst = static_cast<uint16_t*>(v_cache);
+      c.src_st = tok_stride;
+      c.src_sb = tok_stride * n_static;
+      c.B = B;
+      c.H = H;
+      c.D = D;
+      c.n_cached = int32_t(n_cached);
+      c.n_copy = n_copy;
+      for (int i = 0; i < n_copy; ++i) c.seg[i] = seg[i];
+      c.total_rows = int32_t(n_cached);
+    }
+    // cache store: one thread per 16-byte granule, 256 per work-group
+    RC_TRY(check_blocks((int64_t(B) * H * n_cached * (D / 8) + 255) / 256, "cache store"));
+    RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
+    if (n_cached > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
+    return RC_OK;
+  }
+  CacheStore8Params c;
+  memset(&c, 0, sizeof c);
+  c.k_src = static_cast<const uint16_t*>(k_static);
+  c.v_src = static_cast<const uint16_t*>(v_static);
+  c.k_dst = static_cast<uint8_t*>(k_cache);
+  c.vt_dst = static_cast<uint8_t*>(v_cache);
+  c.kv_scale = kv_scale;
+  c.src_st = tok_stride;
+  c.src_sb = tok_stride * n_static;
+  c.B = B;
+  c.H = H;
+  c.D = D;
+  c.n_pad = int32_t(n_pad);
+  c.n_copy = n_copy;
+  for (int i = 0; i < n_copy; ++i) c.seg[i] = seg[i];
+  c.total_rows = int32_t(n_cached);
+  // the quantising store's grids: (B H) x padded-row blocks, one thread per K8 granule
+  RC_TRY(check_blocks(int64_t(B) * H, "FP8 cache store"));
+  RC_TRY(check_blocks((int64_t(B) * H * n_pad * (D / 8) + 255) / 256, "FP8 cache store"));
   RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
-  if (n_cached > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
+  if (n_cached > 0) RC_TRY(hip_status(launch_cache_store_fp8(c, stream), "FP8 cache store launch"));
   return RC_OK;
 }
 
-int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D) {
-  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 1;
-  if (B < 1 || H < 1 || (D != 64 && D != 128)) return 1;
-  Params p;
-  memset(&p, 0, sizeof p);
-  p.B = B;
-  p.H = H;
-  if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
-  return auto_splits(p);
-}
-
-size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
-  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
-  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsBalanced) return 0;
-  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
-  if (splits == kSplitsBalanced) return balanced_workspace_bytes(D);
-  if (splits <= 1) return 0;
-  const int64_t n_live = count_rows(L, RowSet::Live);
-  return size_t(splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
-}
-
-rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
-                                   const void* q_live, const void* k_live, const void* v_live,
-                                   int64_t tok_stride, const void* k_cache, const void* v_cache,
-                                   void* o_live, float* lse_live, int32_t splits, void* workspace,
-                                   size_t ws_bytes, void* stream) {
+// The per-step attention over either cache format (bf16, or FP8: K8 and the
+// transposed V8 with their scales).
+rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q_live,
+                    const void* k_live, const void* v_live, int64_t tok_stride, bool fp8, const void* k_cache,
+                    const void* v_cache, const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
+                    void* workspace, size_t ws_bytes, void* stream) {
   RC_TRY(check_layout(L, RC_ENTRY_STEP));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
@@ -211,6 +239,11 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   }
   const int64_t n_live = count_rows(L, RowSet::Live);
   const int64_t n_cached = count_cached_rows(L);
+  const int64_t n_pad = count_cached_rows_aligned(L, kFp8Align);
+  if (fp8 && splits == kSplitsBalanced) {
+    set_error("the balanced schedule is not available with the FP8 cache");
+    return RC_ERR_UNSUPPORTED;
+  }
   if (n_live == 0) return RC_OK;  // no LT/X segment: nothing to attend
   RC_TRY(check_ptr(q_live, "q_live"));
   RC_TRY(check_ptr(k_live, "k_live"));
@@ -218,14 +251,28 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   RC_TRY(check_ptr(o_live, "o_live"));
   RC_TRY(check_lse(lse_live, "lse_live"));
   if (n_cached > 0) {
-    RC_TRY(check_ptr(k_cache, "k_cache"));
-    RC_TRY(check_ptr(v_cache, "v_cache"));
+    RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
+    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8t" : "v_cache"));
+    if (fp8) {
+      if (!kv_scale) {
+        set_error("kv_scale is null");
+        return RC_ERR_ARG;
+      }
+      RC_TRY(check_lse(kv_scale, "kv_scale"));
+      if (n_pad > (int64_t(1) << 22)) {
+        set_error("FP8 cache of %lld keys per (batch, head) exceeds 2^22", (long long)n_pad);
+        return RC_ERR_ARG;
+      }
+    }
   }
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
-  RC_TRY(plan(L, RC_ENTRY_STEP, p));
-  p.splits = splits == 0 ? auto_splits(p) : splits;
+  RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8 ? kFp8Align : 1));
+  // the automatic choice is the one rc_step_auto_splits reports (from the
+  // unpadded plan, which the FP8 padding can change by a few key tiles)
+  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
+  p.splits = splits;
   const bool balanced = p.splits == kSplitsBalanced;
   if (balanced) {
     p.units = int64_t(B) * H * p.units_bh;
@@ -240,10 +287,15 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   p.o_st = int64_t(H) * D;
   p.o_sb = p.o_st * n_live;
   p.lse = lse_live;
-  p.src[0] = KeySrc{static_cast<const uint16_t*>(k_live), static_cast<const uint16_t*>(v_live),
-                    tok_stride * n_live, D, tok_stride};
-  p.src[1] = KeySrc{static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache),
-                    int64_t(H) * n_cached * D, n_cached * D, D};
+  p.src[0] = bf16_source(k_live, v_live, tok_stride * n_live, D, tok_stride);
+  if (fp8) {
+    p.fp8 = 1;
+    p.kv_scale = kv_scale;
+    p.src[1] = KeySrc{static_cast<const char*>(k_cache), static_cast<const char*>(v_cache), int64_t(H) * n_pad * D,
+                      n_pad * D, D, int64_t(H) * D * n_pad, D * n_pad, 1, n_pad};
+  } else {
+    p.src[1] = bf16_source(k_cache, v_cache, int64_t(H) * n_cached * D, n_cached * D, D);
+  }
   if (balanced) {
     const size_t need = balanced_workspace_bytes(D);
     if (!workspace || !aligned16(workspace) || ws_bytes < need) {
@@ -288,6 +340,68 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
   return RC_OK;
 }
 
+}  // namespace
+}  // namespace rc
+
+using namespace rc;
+
+extern "C" {
+
+rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                            const void* q_static, const void* k_static, const void* v_static,
+                            int64_t tok_stride, void* o_static, float* lse_static, void* k_cache,
+                            void* v_cache, void* stream) {
+  return prefill_impl(L, B, H, D, scale, q_static, k_static, v_static, tok_stride, o_static, lse_static, false,
+                      k_cache, v_cache, nullptr, stream);
+}
+
+rc_status rc_ref_kv_prefill_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                const void* q_static, const void* k_static, const void* v_static,
+                                int64_t tok_stride, void* o_static, float* lse_static, void* k_cache8,
+                                void* v_cache8t, float* kv_scale, void* stream) {
+  return prefill_impl(L, B, H, D, scale, q_static, k_static, v_static, tok_stride, o_static, lse_static, true,
+                      k_cache8, v_cache8t, kv_scale, stream);
+}
+
+int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D) {
+  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 1;
+  if (B < 1 || H < 1 || (D != 64 && D != 128)) return 1;
+  Params p;
+  memset(&p, 0, sizeof p);
+  p.B = B;
+  p.H = H;
+  if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
+  return auto_splits(p);
+}
+
+size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
+  if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
+  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsBalanced) return 0;
+  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
+  if (splits == kSplitsBalanced) return balanced_workspace_bytes(D);
+  if (splits <= 1) return 0;
+  const int64_t n_live = count_rows(L, RowSet::Live);
+  return size_t(splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
+}
+
+rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                   const void* q_live, const void* k_live, const void* v_live,
+                                   int64_t tok_stride, const void* k_cache, const void* v_cache,
+                                   void* o_live, float* lse_live, int32_t splits, void* workspace,
+                                   size_t ws_bytes, void* stream) {
+  return step_impl(L, B, H, D, scale, q_live, k_live, v_live, tok_stride, false, k_cache, v_cache, nullptr, o_live,
+                   lse_live, splits, workspace, ws_bytes, stream);
+}
+
+rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                       const void* q_live, const void* k_live, const void* v_live,
+                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8t,
+                                       const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
+                                       void* workspace, size_t ws_bytes, void* stream) {
+  return step_impl(L, B, H, D, scale, q_live, k_live, v_live, tok_stride, true, k_cache8, v_cache8t, kv_scale,
+                   o_live, lse_live, splits, workspace, ws_bytes, stream);
+}
+
 rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q,
                             const void* k, const void* v, int64_t tok_stride, void* o, float* lse,
                             void* stream) {
@@ -312,8 +426,7 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   p.o_st = int64_t(H) * D;
   p.o_sb = p.o_st * n;
   p.lse = lse;
-  p.src[0] = KeySrc{static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), tok_stride * n, D,
-                    tok_stride};
+  p.src[0] = bf16_source(k, v, tok_stride * n, D, tok_stride);
   RC_TRY(hip_status(launch_attention(p, D, stream), "full attention launch"));
   return RC_OK;
 }

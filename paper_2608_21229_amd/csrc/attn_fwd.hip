@@ -75,10 +75,11 @@ __device__ __forceinline__ float sum_halves(float x) {
 // source descriptors in the kernel arguments are read again only when the
 // cursor crosses into the next range.
 struct Cursor {
-  const uint16_t* k;  // K / V of the current tile's first key, batch and head applied
-  const uint16_t* v;
-  int64_t step;       // elements between consecutive tiles of the range (kBN * st)
-  int32_t st;         // token stride of the key source (elements)
+  const char* k;      // K / V of the current tile's first key, batch and head applied (bytes)
+  const char* v;
+  int64_t kstep;      // bytes between consecutive tiles of the range, K and V
+  int64_t vstep;
+  int32_t st;         // K token stride of the key source (bytes)
   int32_t rem;        // keys of the range from the current tile on
   int32_t src;        // key source of the range
   int32_t r, t, ntiles, r_end;
@@ -92,12 +93,13 @@ __device__ __forceinline__ void cursor_load(const Params& p, Cursor& c, int r, i
   c.t = t;
   c.ntiles = rg.ntiles;
   c.src = rg.src;
-  c.st = int32_t(s.st);
+  c.st = int32_t(s.k_st);
   c.rem = rg.len - t * kBN;
-  c.step = int64_t(kBN) * s.st;
-  const int64_t base = int64_t(c.b) * s.sb + int64_t(c.h) * s.sh + int64_t(rg.start + t * kBN) * s.st;
-  c.k = s.k + base;
-  c.v = s.v + base;
+  c.kstep = int64_t(kBN) * s.k_st;
+  c.vstep = int64_t(kBN) * s.v_st;
+  const int64_t key = rg.start + t * kBN;
+  c.k = s.k + int64_t(c.b) * s.k_sb + int64_t(c.h) * s.k_sh + key * s.k_st;
+  c.v = s.v + int64_t(c.b) * s.v_sb + int64_t(c.h) * s.v_sh + key * s.v_st;
 }
 
 __device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int kt, int b, int h) {
@@ -107,7 +109,7 @@ __device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int
   c.r_end = qs.r0 + qs.nr;
   if (qs.nr == 0) {  // a query segment that reads no key: no tile, and no range entry to read
     c.k = c.v = nullptr;
-    c.step = 0;
+    c.kstep = c.vstep = 0;
     c.st = c.rem = c.src = 0;
     c.r = qs.r0;
     c.t = c.ntiles = 0;
@@ -126,8 +128,8 @@ __device__ __forceinline__ Cursor cursor_at(const Params& p, const QSeg& qs, int
 
 __device__ __forceinline__ void cursor_next(const Params& p, Cursor& c) {
   if (++c.t < c.ntiles) {
-    c.k += c.step;
-    c.v += c.step;
+    c.k += c.kstep;
+    c.v += c.vstep;
     c.rem -= kBN;
   } else if (c.r + 1 < c.r_end) {
     cursor_load(p, c, c.r + 1, 0);
@@ -200,7 +202,7 @@ __device__ __forceinline__ void issue_tile(const Cursor& c, int wave, const uint
                                            uint16_t* ks, uint16_t* vs) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
   const int valid = min(kBN, c.rem);
-  const int nrec = valid * c.st * 2;
+  const int nrec = valid * c.st;
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
   // the lane offsets are passed straight from the long-lived per-source
@@ -266,21 +268,24 @@ __device__ __forceinline__ void s_part(const uint16_t* ks, int lane, const bf16x
 }
 
 // Online softmax of one S^T tile (row = this lane's query) into P^T (bf16).
-template <int D>
+template <int D, bool kNaturalKeys = false>
 __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)[2], bf16x8 (&pf)[4],
                                              f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float c) {
   constexpr int NB = D / 32;
   const int hh = lane >> 5;
   // ragged tail: keys past the end of the range score -inf.  Slot r of half
-  // hh holds key kb*32 + 8 (r/4) + 4 hh + r%4: compare the lane-independent
-  // part against valid - 4 hh.
+  // hh holds key kb*32 + 8 (r/4) + 4 hh + r%4 (kb*32 + 16 (r/8) + 8 hh + r%8
+  // for FP8 cache tiles, whose K rows are permuted): compare the
+  // lane-independent part against valid - 4 hh (valid - 8 hh).
   if (valid < kBN) {
-    const int lim = valid - 4 * hh;
+    const int lim = valid - (kNaturalKeys ? 8 : 4) * hh;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (kb * 32 + 8 * (r >> 2) + (r & 3) >= lim) sacc[kb][r] = -INFINITY;
+      for (int r = 0; r < 16; ++r) {
+        const int key = kNaturalKeys ? kb * 32 + 16 * (r >> 3) + (r & 7) : kb * 32 + 8 * (r >> 2) + (r & 3);
+        if (key >= lim) sacc[kb][r] = -INFINITY;
+      }
   }
   float mx = sacc[0][0];
 #pragma unroll
@@ -361,6 +366,127 @@ __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t*
   pv_part<D>(vs, lane, pf, oacc);
 }
 
+// ---------------------------------------------------------------- FP8 cache tiles
+// A cached tile from the FP8 cache sits in LDS as K8 (64 key rows of D bytes,
+// 16-byte granule g of row r at slot g ^ ((r >> 1) & (D/16 - 1))) and V8t
+// (D rows of 64 key bytes, granule g of row d at slot g ^ ((d >> 2) & 3)).
+// Fragments are widened to bf16 with the power-of-two scale, which is exact,
+// so the MFMAs are those of the bf16 path.  K fragment rows are permuted by
+// pi (keys 4-7 <-> 8-11 within each 16) so that the S^T accumulator holds, in
+// each 32-lane half, 8 consecutive keys per 16-key chunk: the V^T fragment of
+// a chunk is then one 8-byte read of a V8t row.
+struct Fp8Ctx {
+  float sk, sv;          // scales of this (batch, head)
+  uint32_t voffk, voffv; // this lane's byte offsets of its granule in a K8 / V8t tile
+  bool loads;            // this wave loads a granule of each tile (D/16 waves do)
+};
+
+__device__ __forceinline__ int kpi(int x) { return (((x >> 2) ^ (x >> 3)) & 1) ? x ^ 12 : x; }
+
+__device__ __forceinline__ bf16x8 widen8(u32x2 w, float s) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], s, false);
+  const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], s, true);
+  const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], s, false);
+  const bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], s, true);
+  return bf16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+// K fragment f = kb * NDC + dc: row kb*32 + pi(lane%32), bytes 16 dc + 8 (lane/32) .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 k_frag8(const char* ks, int lane, int f, float s) {
+  constexpr int NDC = D / 16;
+  const int kb = f / NDC, dc = f % NDC;
+  const int row = kb * 32 + kpi(lane & 31);
+  const int off = row * D + ((dc ^ ((row >> 1) & (NDC - 1))) << 4) + 8 * (lane >> 5);
+  return widen8(*reinterpret_cast<const u32x2*>(ks + off), s);
+}
+
+// V^T fragment f = cc * NB + nb: row d = 32 nb + lane%32, keys 16 cc + 8 (lane/32) .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 v_frag8(const char* vs, int lane, int f, float s) {
+  constexpr int NB = D / 32;
+  const int cc = f / NB, nb = f % NB;
+  const int d = nb * 32 + (lane & 31);
+  const int off = d * 64 + ((cc ^ ((d >> 2) & 3)) << 4) + 8 * (lane >> 5);
+  return widen8(*reinterpret_cast<const u32x2*>(vs + off), s);
+}
+
+template <int D>
+__device__ __forceinline__ void s_part8(const char* ks, int lane, const bf16x8 (&qf)[D / 16], f32x16 (&sacc)[2],
+                                        float sk) {
+  constexpr int NDC = D / 16;
+  constexpr int NF = 2 * NDC;
+  constexpr int PF = kPrefetch;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+  bf16x8 a[PF + 1];
+#pragma unroll
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = k_frag8<D>(ks, lane, f, sk);
+  sched_fence();
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int kb = f / NDC, dc = f % NDC;
+    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], qf[dc], sacc[kb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = k_frag8<D>(ks, lane, f + PF, sk);
+    sched_fence();
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void pv_part8(const char* vs, int lane, const bf16x8 (&pf)[4], f32x16 (&oacc)[D / 32],
+                                         float sv) {
+  constexpr int NB = D / 32;
+  constexpr int NF = 4 * NB;
+  constexpr int PF = kPrefetch;
+  bf16x8 a[PF + 1];
+#pragma unroll
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag8<D>(vs, lane, f, sv);
+  sched_fence();
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int cc = f / NB, nb = f % NB;
+    oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], pf[cc], oacc[nb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = v_frag8<D>(vs, lane, f + PF, sv);
+    sched_fence();
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void tile_compute8(const char* ks, const char* vs, int lane, int valid,
+                                              const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
+                                              float& lsum, float c, const Fp8Ctx& f8) {
+  f32x16 sacc[2];
+  bf16x8 pf[4];
+  s_part8<D>(ks, lane, qf, sacc, f8.sk);
+  softmax_part<D, true>(lane, valid, sacc, pf, oacc, m_used, lsum, c);
+  pv_part8<D>(vs, lane, pf, oacc, f8.sv);
+}
+
+// The DMA of one FP8 cache tile: one 16-byte granule of K8 and one of V8t per
+// lane of the first D/16 waves.  K8 rows past the range end lie beyond the
+// record count and arrive as zeros; V8t bytes past the range end within a d
+// row are other cached keys or zero padding (finite, and their weight is 0).
+// The record count covers the last d row up to the next 16-key boundary: the
+// range check works on whole dwords, so a count ending inside a dword would
+// zero valid keys of that row; tiles start on 16-key boundaries and the padded
+// key count is a multiple of 16, so the rounded count stays inside the plane.
+template <int D>
+__device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, const Fp8Ctx& f8, int64_t v_row, char* ks,
+                                            char* vs) {
+  if (!f8.loads) return;
+  const int valid = min(kBN, c.rem);
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, valid * D, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, int(int64_t(D - 1) * v_row + ((valid + 15) & ~15)),
+                                        0x00020000);
+  dma16(lds_addr(reinterpret_cast<const uint16_t*>(ks + wave * 1024)), f8.voffk, rk);
+  dma16(lds_addr(reinterpret_cast<const uint16_t*>(vs + wave * 1024)), f8.voffv, rv);
+}
+
 // Wait until at most `n` tiles of this wave's DMA loads are still in flight
 // (each tile is 2 * kLoads vector-memory instructions per wave).
 template <int kLoads>
@@ -384,23 +510,80 @@ struct RingState {
 
 // Tile k (in stage S): wait for its DMA, barrier, refill the stage that
 // became free with tile k + kStages - 1, then compute tile k.
-template <int S, int D>
+// Issue tile c into stage S; kF8: the tiles of this ring are FP8 cache tiles.
+template <int S, int D, bool kF8>
+__device__ __forceinline__ void issue_any(const Params& p, const Cursor& c, int wave, const uint32_t* voff0,
+                                          const uint32_t* voff1, const Fp8Ctx& f8) {
+  if constexpr (kF8)
+    issue_tile8<D>(c, wave, f8, p.src[1].v_row, reinterpret_cast<char*>(kbuf<S>()),
+                   reinterpret_cast<char*>(vbuf<S>()));
+  else
+    issue_tile<D>(c, wave, voff0, voff1, kbuf<S>(), vbuf<S>());
+}
+
+template <int S, int D, bool kF8>
 __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, int b, int h, int wave, int lane,
                                           bool wave_active, const uint32_t* voff0, const uint32_t* voff1,
                                           RingState<D>& rs, const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
-                                          float& m_used, float& lsum, float c) {
+                                          float& m_used, float& lsum, float c, const Fp8Ctx& f8) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
   constexpr int F = (S + kStages - 1) % kStages;  // stage freed by the previous tile
+  // with two stages this is vmcnt(0): only tile k's loads are in flight here
+  static_assert(!kF8 || kStages == 2, "FP8 tiles issue fewer loads: the in-flight count assumes two stages");
   wait_tiles_in_flight<kLoads>(rs.issued - 1 - k);
   ring_barrier();
   if (rs.issued < kt_end) {
-    issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<F>(), vbuf<F>());
+    issue_any<F, D, kF8>(p, rs.icur, wave, voff0, voff1, f8);
     ++rs.issued;
     if (rs.issued < kt_end) cursor_next(p, rs.icur);
   }
   const int valid = tile_valid(rs.ccur);
-  if (wave_active) tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
+  if (wave_active) {
+    if constexpr (kF8)
+      tile_compute8<D>(reinterpret_cast<const char*>(kbuf<S>()), reinterpret_cast<const char*>(vbuf<S>()), lane,
+                       valid, qf, oacc, m_used, lsum, c, f8);
+    else
+      tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
+  }
   if (k + 1 < kt_end) cursor_next(p, rs.ccur);
+}
+
+// The K/V ring over key tiles [kt_begin, kt_end) of query segment qs: tile kt
+// lives in stage (kt - kt_begin) % kStages; tiles up to kStages - 1 ahead are in
+// flight while one is computed.  kF8: the tiles are FP8 cache tiles.
+template <int D, bool kF8>
+__device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
+                                         int wave, int lane, bool wave_active, const uint32_t* voff0,
+                                         const uint32_t* voff1, const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
+                                         float& m_used, float& lsum, float c, const Fp8Ctx& f8) {
+  if (kt_begin >= kt_end) return;
+  RingState<D> rs;
+  rs.icur = cursor_at(p, qs, kt_begin, b, h);
+  rs.ccur = rs.icur;
+  rs.issued = kt_begin;
+  if (rs.issued < kt_end) {
+    issue_any<0, D, kF8>(p, rs.icur, wave, voff0, voff1, f8);
+    if (++rs.issued < kt_end) cursor_next(p, rs.icur);
+  }
+  if constexpr (kStages > 2) {
+    if (rs.issued < kt_end) {
+      issue_any<1, D, kF8>(p, rs.icur, wave, voff0, voff1, f8);
+      if (++rs.issued < kt_end) cursor_next(p, rs.icur);
+    }
+  }
+  for (int kt = kt_begin; kt < kt_end; kt += kStages) {
+    ring_step<0, D, kF8>(p, kt, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c,
+                         f8);
+    if (kt + 1 >= kt_end) break;
+    ring_step<1, D, kF8>(p, kt + 1, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum,
+                         c, f8);
+    if constexpr (kStages > 2) {
+      if (kt + 2 >= kt_end) break;
+      ring_step<2, D, kF8>(p, kt + 2, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used,
+                           lsum, c, f8);
+    }
+  }
+
 }
 
 // Logical work-group index: the hardware deals blocks round-robin to the 8
@@ -416,7 +599,7 @@ __device__ __forceinline__ int xcd_logical_block(int bid, int nblk) {
 // tiles [kt_begin, kt_end).  part_row < 0: final output (bf16 O and LSE);
 // otherwise unnormalised fp32 partials (O, running max in log2 units, row
 // sum) at workspace row part_row + (row inside the tile).
-template <int D>
+template <int D, bool kF8>
 __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int t, int b, int h, int kt_begin,
                                             int kt_end, int64_t part_row, int wave, int lane) {
   constexpr int GR = D / 8;
@@ -439,8 +622,21 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
     const int pos = (i * kWaves + wave) * 64 + lane;
     const int row = pos / GR, slot = pos % GR;
     const uint32_t g16 = uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
-    voff0[i] = uint32_t(row) * uint32_t(p.src[0].st) * 2u + g16;
-    voff1[i] = uint32_t(row) * uint32_t(p.src[1].st) * 2u + g16;
+    voff0[i] = uint32_t(row) * uint32_t(p.src[0].k_st) + g16;
+    voff1[i] = uint32_t(row) * uint32_t(p.src[1].k_st) + g16;
+  }
+  // FP8 cache tiles: scales of this (batch, head) and this lane's granule offsets
+  Fp8Ctx f8{};
+  if constexpr (kF8) {
+    constexpr int NDCk = D / 16;
+    f8.sk = p.kv_scale[(int64_t(b) * p.H + h) * 2];
+    f8.sv = p.kv_scale[(int64_t(b) * p.H + h) * 2 + 1];
+    f8.loads = wave < NDCk;
+    const int pidx = wave * 64 + lane;
+    const int krow = pidx / NDCk, kslot = pidx % NDCk;
+    f8.voffk = uint32_t(krow * D + ((kslot ^ ((krow >> 1) & (NDCk - 1))) << 4));
+    const int drow = pidx >> 2, vslot = pidx & 3;
+    f8.voffv = uint32_t(int64_t(drow) * p.src[1].v_row + ((vslot ^ ((drow >> 2) & 3)) << 4));
   }
 
   // ---- Q fragment (B operand of S^T = K Q^T): lane holds query (lane % 32),
@@ -470,31 +666,20 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
   float lsum = 0.f;          // this half's partial row sum
   const float c = p.scale_log2;
 
-  // ---- K/V ring: tile kt lives in stage (kt - kt_begin) % kStages; tiles up
-  // to kStages - 1 ahead are in flight while one is computed.
-  RingState<D> rs;
-  rs.icur = cursor_at(p, qs, kt_begin, b, h);
-  rs.ccur = rs.icur;
-  rs.issued = kt_begin;
-  if (rs.issued < kt_end) {
-    issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<0>(), vbuf<0>());
-    if (++rs.issued < kt_end) cursor_next(p, rs.icur);
-  }
-  if constexpr (kStages > 2) {
-    if (rs.issued < kt_end) {
-      issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<1>(), vbuf<1>());
-      if (++rs.issued < kt_end) cursor_next(p, rs.icur);
-    }
-  }
-  for (int kt = kt_begin; kt < kt_end; kt += kStages) {
-    ring_step<0, D>(p, kt, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
-    if (kt + 1 >= kt_end) break;
-    ring_step<1, D>(p, kt + 1, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
-    if constexpr (kStages > 2) {
-      if (kt + 2 >= kt_end) break;
-      ring_step<2, D>(p, kt + 2, kt_end, b, h, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum,
-                      c);
-    }
+  if constexpr (kF8) {
+    // the planner puts this segment's fresh (bf16) key ranges before its FP8
+    // cache ranges: one ring over each kind
+    int kt_split = 0;
+    for (int r = qs.r0; r < qs.r0 + qs.nr && p.range[r].src == 0; ++r) kt_split += p.range[r].ntiles;
+    const int mid = min(max(kt_split, kt_begin), kt_end);
+    run_ring<D, false>(p, qs, b, h, kt_begin, mid, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c,
+                       f8);
+    if (kt_begin < mid && mid < kt_end) ring_barrier();  // the first ring's stages are read no more
+    run_ring<D, true>(p, qs, b, h, mid, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c,
+                      f8);
+  } else {
+    run_ring<D, false>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum,
+                       c, f8);
   }
 
   // ---- epilogue
@@ -536,7 +721,7 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
 }
 
 // One work-group per (batch, head, query tile, key split).
-template <int D, bool kSplit>
+template <int D, bool kSplit, bool kF8>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -555,7 +740,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   int64_t part_row = -1;
   if constexpr (kSplit)
     part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * kBM;
-  attend_tile<D>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
+  attend_tile<D, kF8>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
 }
 
 // Balanced schedule: work-group g of G takes the key-tile units
@@ -563,7 +748,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
 // segment, query tile, key tile).  A query tile wholly inside one range is
 // written directly; a cut one leaves partials: the work-group's first piece
 // in workspace slot 2 g, its last piece (when not also its first) in 2 g + 1.
-template <int D>
+template <int D, bool kF8>
 __global__ __launch_bounds__(kThreads) void attn_fwd_balanced_kernel(const Params p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -585,7 +770,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_balanced_kernel(const Param
     const bool whole = kt0 == 0 && kt1 == qs.ktiles;
     const int64_t part_row = whole ? -1 : int64_t(first ? 2 * g : 2 * g + 1) * kBM;
     if (!first) ring_barrier();  // every wave is done with the previous piece's LDS stages
-    attend_tile<D>(p, qs, qs.tile0 + tl, int(bh / p.H), int(bh % p.H), kt0, kt1, part_row, wave, lane);
+    attend_tile<D, kF8>(p, qs, qs.tile0 + tl, int(bh / p.H), int(bh % p.H), kt0, kt1, part_row, wave, lane);
     u += kt1 - kt0;
     first = false;
   }
@@ -716,26 +901,28 @@ __global__ __launch_bounds__(256) void cache_store_kernel(const CacheStoreParams
 
 }  // namespace
 
+template <int D, bool kF8>
+void launch_grid(const Params& p, int64_t blocks, hipStream_t s) {
+  if (p.splits > 1) hipLaunchKernelGGL((attn_fwd_kernel<D, true, kF8>), dim3(blocks), dim3(kThreads), 0, s, p);
+  else hipLaunchKernelGGL((attn_fwd_kernel<D, false, kF8>), dim3(blocks), dim3(kThreads), 0, s, p);
+}
+
 int launch_attention(const Params& p, int D, void* stream) {
   const int64_t blocks = int64_t(p.B) * p.H * p.n_qtiles * p.splits;
   if (blocks == 0) return 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool split = p.splits > 1;
-  if (D == 128) {
-    if (split) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), dim3(blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, s, p);
-  } else {
-    if (split) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, p);
-  }
+  if (D == 128) p.fp8 ? launch_grid<128, true>(p, blocks, s) : launch_grid<128, false>(p, blocks, s);
+  else p.fp8 ? launch_grid<64, true>(p, blocks, s) : launch_grid<64, false>(p, blocks, s);
   return int(hipGetLastError());
 }
 
 int launch_attention_balanced(const Params& p, int D, void* stream) {
   if (p.units == 0) return 0;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (D == 128) hipLaunchKernelGGL(attn_fwd_balanced_kernel<128>, dim3(p.bal_wgs), dim3(kThreads), 0, s, p);
-  else hipLaunchKernelGGL(attn_fwd_balanced_kernel<64>, dim3(p.bal_wgs), dim3(kThreads), 0, s, p);
+  // bf16 caches only (the API refuses the balanced schedule with the FP8 cache)
+  const dim3 g(p.bal_wgs), t(kThreads);
+  if (D == 128) hipLaunchKernelGGL((attn_fwd_balanced_kernel<128, false>), g, t, 0, s, p);
+  else hipLaunchKernelGGL((attn_fwd_balanced_kernel<64, false>), g, t, 0, s, p);
   return int(hipGetLastError());
 }
 

@@ -1,0 +1,193 @@
+// FP8 (e4m3fn) reference cache store: quantise the cached segments' K/V rows
+// of the static buffers into K8 [B, H, N_pad, D] and transposed V8 [B, H, D,
+// N_pad] with one power-of-two scale per (batch, head) and tensor.
+//
+// Per (b, h) and tensor X: amax = max |x| over the cached rows; the scale is
+// s = 2^e with e the smallest integer such that amax / s <= 448 (the largest
+// finite e4m3fn value), s = 1 when amax = 0; the code of x is the nearest
+// e4m3fn value of x / s (ties to even), which the hardware conversion
+// computes.  Dividing by a power of two is exact, so a code depends on x alone,
+// and code * s is exact in bf16.  Cached segments start at multiples of 16
+// keys; padding keys hold zeros.
+//
+// Four launches on the stream: amax accumulators cleared, per-(b, h) amax
+// (work-group maxima, then one atomic max per work-group and tensor: the
+// result does not depend on the order), the two quantising stores, and the
+// scales written over the amax values.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rc_internal.h"
+
+namespace rc {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kRowsPerBlock = 256;
+
+// e: the smallest integer with amax * 2^-e <= 448 (amax = m 2^k, 0.5 <= m < 1;
+// 448 = 0.875 * 2^9).
+__device__ __forceinline__ int fp8_exponent(float amax) {
+  if (!(amax > 0.f)) return 0;
+  int k;
+  const float m = frexpf(amax, &k);
+  return m <= 0.875f ? k - 9 : k - 8;
+}
+
+// Source row of padded cache position pos, or -1 for a padding position.
+__device__ __forceinline__ int source_row(const CacheStore8Params& c, int pos) {
+  for (int i = 0; i < c.n_copy; ++i) {
+    const CopySeg& sg = c.seg[i];
+    if (pos >= sg.dst_row0 && pos < sg.dst_row0 + sg.len) return sg.src_row0 + (pos - sg.dst_row0);
+  }
+  return -1;
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ float amax8(u32x4 g) {
+  float m = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m = fmaxf(m, fabsf(bf16_bits_to_float(g[i] & 0xffffu)));
+    m = fmaxf(m, fabsf(bf16_bits_to_float(g[i] >> 16)));
+  }
+  return m;
+}
+
+// 8 bf16 values (one 16-byte granule) times 2^-e to 8 e4m3fn codes.
+__device__ __forceinline__ u32x2 quant8(u32x4 g, int e) {
+  u32x2 out;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float a = ldexpf(bf16_bits_to_float(g[2 * i] & 0xffffu), -e);
+    const float b = ldexpf(bf16_bits_to_float(g[2 * i] >> 16), -e);
+    const float cc = ldexpf(bf16_bits_to_float(g[2 * i + 1] & 0xffffu), -e);
+    const float d = ldexpf(bf16_bits_to_float(g[2 * i + 1] >> 16), -e);
+    int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+    w = __builtin_amdgcn_cvt_pk_fp8_f32(cc, d, w, true);
+    out[i] = uint32_t(w);
+  }
+  return out;
+}
+
+__global__ void fill_zero_kernel(float* a, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) a[i] = 0.f;
+}
+
+// Grid (B * H, ceil(n_pad / kRowsPerBlock)); 256 threads stride over the
+// block's rows x D/8 granules of K and V.
+__global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
+  const int bh = blockIdx.x, b = bh / c.H, h = bh % c.H;
+  const int gr = c.D / 8;
+  const int row0 = blockIdx.y * kRowsPerBlock;
+  float mk = 0.f, mv = 0.f;
+  for (int g = threadIdx.x; g < kRowsPerBlock * gr; g += blockDim.x) {
+    const int pos = row0 + g / gr;
+    if (pos >= c.n_pad) break;
+    const int srow = source_row(c, pos);
+    if (srow < 0) continue;
+    const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + (g % gr) * 8;
+    mk = fmaxf(mk, amax8(*reinterpret_cast<const u32x4*>(c.k_src + off)));
+    mv = fmaxf(mv, amax8(*reinterpret_cast<const u32x4*>(c.v_src + off)));
+  }
+  __shared__ float red[2][256];
+  red[0][threadIdx.x] = mk;
+  red[1][threadIdx.x] = mv;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      red[0][threadIdx.x] = fmaxf(red[0][threadIdx.x], red[0][threadIdx.x + w]);
+      red[1][threadIdx.x] = fmaxf(red[1][threadIdx.x], red[1][threadIdx.x + w]);
+    }
+    __syncthreads();
+  }
+  // non-negative floats order like their bit patterns
+  if (threadIdx.x == 0) {
+    atomicMax(reinterpret_cast<unsigned int*>(c.kv_scale + bh * 2), __float_as_uint(red[0][0]));
+    atomicMax(reinterpret_cast<unsigned int*>(c.kv_scale + bh * 2 + 1), __float_as_uint(red[1][0]));
+  }
+}
+
+// K8: one thread per (b, h, padded row, granule of 8 elements).
+__global__ __launch_bounds__(256) void quant_k_kernel(const CacheStore8Params c) {
+  const int gr = c.D / 8;
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t total = int64_t(c.B) * c.H * c.n_pad * gr;
+  if (idx >= total) return;
+  const int g = int(idx % gr);
+  int64_t rest = idx / gr;
+  const int pos = int(rest % c.n_pad);
+  const int64_t bh = rest / c.n_pad;
+  const int b = int(bh / c.H), h = int(bh % c.H);
+  const int srow = source_row(c, pos);
+  u32x2 q = {0u, 0u};
+  if (srow >= 0) {
+    const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
+    q = quant8(*reinterpret_cast<const u32x4*>(c.k_src + off), fp8_exponent(c.kv_scale[bh * 2]));
+  }
+  *reinterpret_cast<u32x2*>(c.k_dst + (bh * c.n_pad + pos) * c.D + g * 8) = q;
+}
+
+// V8t: one work-group per (b, h, 64 padded positions): quantise the 64 x D
+// block into LDS as [key][d] codes, then write D rows of 64 (or fewer, at the
+// end) key codes with 16-byte stores.
+__global__ __launch_bounds__(256) void quant_vt_kernel(const CacheStore8Params c) {
+  __shared__ uint8_t tile[64 * 128];
+  const int bh = blockIdx.x, b = bh / c.H, h = bh % c.H;
+  const int pos0 = blockIdx.y * 64;
+  const int gr = c.D / 8;
+  const int e = fp8_exponent(c.kv_scale[bh * 2 + 1]);
+  for (int g = threadIdx.x; g < 64 * gr; g += blockDim.x) {
+    const int key = g / gr, gi = g % gr;
+    const int pos = pos0 + key;
+    const int srow = pos < c.n_pad ? source_row(c, pos) : -1;
+    u32x2 q = {0u, 0u};
+    if (srow >= 0) {
+      const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + gi * 8;
+      q = quant8(*reinterpret_cast<const u32x4*>(c.v_src + off), e);
+    }
+    *reinterpret_cast<u32x2*>(tile + key * c.D + gi * 8) = q;
+  }
+  __syncthreads();
+  const int nkeys = min(64, c.n_pad - pos0);  // a multiple of 16
+  for (int w = threadIdx.x; w < c.D * 4; w += blockDim.x) {
+    const int d = w / 4, kg = w % 4;
+    if (kg * 16 >= nkeys) continue;
+    uint32_t word[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t x = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x |= uint32_t(tile[(kg * 16 + 4 * j + i) * c.D + d]) << (8 * i);
+      word[j] = x;
+    }
+    *reinterpret_cast<u32x4*>(c.vt_dst + (int64_t(bh) * c.D + d) * c.n_pad + pos0 + kg * 16) =
+        u32x4{word[0], word[1], word[2], word[3]};
+  }
+}
+
+__global__ void finalize_scale_kernel(float* a, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) a[i] = ldexpf(1.f, fp8_exponent(a[i]));
+}
+
+}  // namespace
+
+int launch_cache_store_fp8(const CacheStore8Params& c, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nsc = c.B * c.H * 2;
+  if (nsc == 0 || c.n_pad == 0) return 0;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((nsc + 255) / 256), dim3(256), 0, s, c.kv_scale, nsc);
+  hipLaunchKernelGGL(amax_kernel, dim3(c.B * c.H, (c.n_pad + kRowsPerBlock - 1) / kRowsPerBlock), dim3(256), 0, s, c);
+  const int64_t tk = int64_t(c.B) * c.H * c.n_pad * (c.D / 8);
+  hipLaunchKernelGGL(quant_k_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c);
+  hipLaunchKernelGGL(quant_vt_kernel, dim3(c.B * c.H, (c.n_pad + 63) / 64), dim3(256), 0, s, c);
+  hipLaunchKernelGGL(finalize_scale_kernel, dim3((nsc + 255) / 256), dim3(256), 0, s, c.kv_scale, nsc);
+  return int(hipGetLastError());
+}
+
+}  // namespace rc

@@ -118,11 +118,19 @@ int64_t count_cached_rows(const rc_layout* L) {
   return n;
 }
 
+int64_t count_cached_rows_aligned(const rc_layout* L, int align) {
+  const uint32_t m = cached_mask(L);
+  int64_t n = 0;
+  for (int i = 0; i < L->n_seg; ++i)
+    if (m >> i & 1u) n = (n + align - 1) / align * align + L->seg[i].len;
+  return (n + align - 1) / align * align;
+}
+
 static RowSet rows_of(int32_t entry) {
   return entry == RC_ENTRY_PREFILL ? RowSet::Static : entry == RC_ENTRY_STEP ? RowSet::Live : RowSet::All;
 }
 
-rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
+rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align) {
   const RowSet rset = rows_of(entry);
   // Position of every segment inside each key source.
   int32_t src_of[RC_MAX_SEGMENTS], pos_of[RC_MAX_SEGMENTS], row_of[RC_MAX_SEGMENTS];
@@ -143,6 +151,7 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
       pos_entry += L->seg[i].len;
     } else if (entry == RC_ENTRY_STEP && (cmask >> i & 1u)) {
       src_of[i] = 1;
+      pos_cache = (pos_cache + cache_align - 1) / cache_align * cache_align;
       pos_of[i] = pos_cache;
       pos_cache += L->seg[i].len;
     }
@@ -171,6 +180,16 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p) {
         tmp[nr].src = src_of[k];
         ++nr;
       }
+    }
+    if (cache_align > 1) {
+      // FP8 cache: fresh (bf16) ranges first, then cache ranges, so that the
+      // kernel runs one ring over each tile kind (softmax is order-free)
+      KeyRange part[RC_MAX_SEGMENTS];
+      int np = 0;
+      for (int pass = 0; pass < 2; ++pass)
+        for (int r = 0; r < nr; ++r)
+          if (tmp[r].src == pass) part[np++] = tmp[r];
+      for (int r = 0; r < nr; ++r) tmp[r] = part[r];
     }
     int ktiles = 0;
     for (int r = 0; r < nr; ++r) {
@@ -300,6 +319,7 @@ int64_t rc_rows(const rc_layout* L, int32_t which) {
     case RC_ROWS_STATIC: return rc::count_rows(L, rc::RowSet::Static);
     case RC_ROWS_LIVE: return rc::count_rows(L, rc::RowSet::Live);
     case RC_ROWS_CACHED: return rc::count_cached_rows(L);
+    case RC_ROWS_CACHED_FP8: return rc::count_cached_rows_aligned(L, rc::kFp8Align);
     case RC_ROWS_ALL: return rc::count_rows(L, rc::RowSet::All);
     default:
       rc::set_error("unknown row class %d", which);

@@ -50,10 +50,16 @@ struct QSeg {
   int32_t ktiles;  // key tiles over all its ranges
 };
 
+// A key source, addressed in bytes.  bf16 sources hold K and V as
+// [B, N, H, D] with one token stride; the FP8 cache holds K as
+// [B, H, N_pad, D] bytes and V transposed as [B, H, D, N_pad] bytes (token
+// stride 1, d rows v_row = N_pad bytes apart).
 struct KeySrc {
-  const uint16_t* k;
-  const uint16_t* v;
-  int64_t sb, sh, st;  // element strides: batch, head, token
+  const char* k;
+  const char* v;
+  int64_t k_sb, k_sh, k_st;  // byte strides of K: batch, head, token
+  int64_t v_sb, v_sh, v_st;  // byte strides of V: batch, head, token
+  int64_t v_row;             // transposed FP8 V: bytes between d rows; 0 otherwise
 };
 
 struct Params {
@@ -66,6 +72,8 @@ struct Params {
   float* ws_ml;        // split partials [splits, B, H, n_rows, 2] (max in log2 units, sum)
   KeySrc src[2];
   int32_t B, H, n_rows, n_qseg, n_qtiles, splits;  // splits: kSplitsBalanced = balanced schedule
+  int32_t fp8;         // key source 1 is the FP8 cache
+  const float* kv_scale;  // FP8 cache: [B, H, 2] power-of-two scales of K and V
   int64_t units_bh;    // key-tile units (query tile x key tile) per (batch, head)
   int64_t units;       // B * H * units_bh
   int32_t bal_wgs;     // work-groups of the balanced schedule
@@ -87,6 +95,21 @@ struct CacheStoreParams {
   int64_t src_sb, src_st;
   int32_t B, H, D, n_cached, n_copy, total_rows;
   CopySeg seg[RC_MAX_SEGMENTS];
+};
+
+// FP8 cache store: quantise the cached segments' K/V rows (bf16, [B, N_static,
+// H, D]) into K8 [B, H, N_pad, D] and transposed V8 [B, H, D, N_pad]; segment
+// positions in the cache are padded to multiples of kFp8Align keys.
+constexpr int kFp8Align = 16;
+struct CacheStore8Params {
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  uint8_t* k_dst;
+  uint8_t* vt_dst;
+  float* kv_scale;     // [B, H, 2]: amax while quantising, the scales afterwards
+  int64_t src_sb, src_st;
+  int32_t B, H, D, n_pad, n_copy, total_rows;
+  CopySeg seg[RC_MAX_SEGMENTS];  // dst_row0: padded position
 };
 
 // Dense projection out = A W^T (+ R) of the chained synthetic layer.
@@ -117,8 +140,9 @@ rc_status check_layout(const rc_layout* L, int32_t entry);  // sets the thread e
 uint32_t cached_mask(const rc_layout* L);                  // bit i: segment i is cached
 int64_t count_rows(const rc_layout* L, RowSet set);
 int64_t count_cached_rows(const rc_layout* L);
+int64_t count_cached_rows_aligned(const rc_layout* L, int align);  // padded cache length
 // Fill p.qseg / p.range / n_qseg / n_qtiles / n_rows for an entry.
-rc_status plan(const rc_layout* L, int32_t entry, Params& p);
+rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align = 1);
 int32_t auto_splits(const Params& p);
 
 void set_error(const char* fmt, ...);
@@ -129,6 +153,7 @@ int launch_combine(const CombineParams& c, void* stream);
 int launch_attention_balanced(const Params& p, int D, void* stream);
 int launch_combine_balanced(const Params& p, int D, void* stream);
 int launch_cache_store(const CacheStoreParams& c, void* stream);
+int launch_cache_store_fp8(const CacheStore8Params& c, void* stream);
 int launch_linear(const LinearParams& q, void* stream);  // linear.hip
 
 }  // namespace rc

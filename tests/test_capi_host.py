@@ -266,3 +266,30 @@ def test_linear_binding_rejects_host_tensors():
     w = torch.zeros(128, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU tensor"):
         rc.linear(a, w)
+
+
+def test_fp8_cache_rows_and_errors():
+    # cached segments start at multiples of 16: ST 5 -> [0, 5), R 33 -> [16, 49), R 7 -> [64, 71); N_pad 80
+    L = rc.Layout([(0, 5), (1, 8), (2, 16), (3, 33), (3, 7)], "perref")
+    assert L.rows(rc.ROWS_CACHED) == 45
+    assert L.rows(rc.ROWS_CACHED_FP8) == 80
+    assert rc.fp8_cache_shapes(L, 2, 3, 64) == ((2, 3, 80, 64), (2, 3, 64, 80), (2, 3, 2))
+    lb = rc.lib()
+    A, U = rc.RC_ERR_ARG, rc.RC_ERR_UNSUPPORTED
+    args = lambda **kw: dict(dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, kc=FAKE, vc=FAKE, sc=FAKE, splits=1), **kw)
+
+    def step8(**kw):
+        a = args(**kw)
+        return lb.rc_step_masked_attention_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, a["q"], a["k"], a["v"], 128,
+                                               a["kc"], a["vc"], a["sc"], a["o"], None, a["splits"], None, 0, None)
+
+    def pre8(**kw):
+        a = args(**kw)
+        return lb.rc_ref_kv_prefill_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, a["q"], a["k"], a["v"], 128, a["o"],
+                                        None, a["kc"], a["vc"], a["sc"], None)
+
+    assert step8(sc=None) == A and pre8(sc=None) == A
+    assert step8(sc=FAKE + 2) == A and pre8(sc=FAKE + 2) == A   # scales need 4-byte alignment
+    assert step8(kc=FAKE + 8) == A and pre8(vc=FAKE + 8) == A    # caches need 16-byte alignment
+    assert step8(splits=-1) == U
+    assert "balanced" in lb.rc_last_error().decode()
