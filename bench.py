@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-STEP_KERNEL = "attn_fwd_kernel<128, false>"
+STEP_KERNEL = "attn_fwd_kernel<128, false, false>"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_21229_amd", "csrc", "attn_fwd.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_fwd_ref5_step_traffic.txt")
 PAPER_CONTEXT = {
