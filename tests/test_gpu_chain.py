@@ -82,6 +82,8 @@ def _bf(shape, seed, std=1.0):
     (127, 384, 128, True, False),
     (129, 128, 256, False, True),
     (1000, 512, 320, True, False),
+    (257, 768, 64, True, True),        # 256-wide tiles: one row past a tile, one K step
+    (2100, 1024, 448, False, False),   # 256-wide tiles: 9 m-tiles (a partial group of 4), odd K steps
 ])
 def test_linear_matches_oracle(M, N, K, resid, strided):
     a_full = _bf((M, K + (64 if strided else 0)), 1 + M)
@@ -113,9 +115,10 @@ def test_linear_in_place_residual():
     check_projection(h, want, "linear in place", f64(a), f64(w), f64(r))
 
 
-def test_linear_rows_do_not_depend_on_batch():
+@pytest.mark.parametrize("N", [384, 512])   # 128-wide and 256-wide output tiles
+def test_linear_rows_do_not_depend_on_batch(N):
     """A row's result is the same bits whatever rows surround it."""
-    M, N, K = 1000, 384, 256
+    M, K = 1000, 256
     a = _bf((M, K), 21).to(DEV)
     w = _bf((N, K), 22, K ** -0.5).to(DEV)
     whole = rc.linear(a, w)

@@ -109,6 +109,16 @@ def test_fp8_ragged(name, segs, D):
     check_fp8_request(wl, "paper")
 
 
+def test_fp8_every_range_length_mod_16():
+    """One cached range of every length 1..17 (and 31, 33, 63): a tile whose last
+    transposed-V row ends inside a dword must still read every valid key."""
+    lens = list(range(1, 18)) + [31, 33, 63]
+    segs = [(0, 16), (1, 16), (2, 64)] + [(3, n) for n in lens]
+    wl = Workload("fp8_lengths", 1, 2, 64, tuple(segs), seed=23)
+    check_fp8_request(wl, "perref", splits=1)
+    check_fp8_request(wl, "isolated", splits=0)
+
+
 def test_fp8_headline():
     """The 5-reference workload at full size (24 heads, 20 544 cached keys), sampled rows."""
     check_fp8_request(workload("ref5"), "perref", every=97)
