@@ -198,8 +198,10 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
  * rc_ref_kv_prefill (o_static, lse_static) and writes the FP8 cache instead of the
  * bf16 one.  rc_step_masked_attention_fp8 is rc_step_masked_attention with the
  * cached K/V read from the FP8 cache (fresh LT/X K/V stay bf16); splits and
- * workspace as there.  Cache pointers 16-byte aligned; kv_scale 4-byte aligned
- * (written by the prefill, read by the step).  Errors as the bf16 entries. */
+ * workspace as there, except that RC_SPLITS_BALANCED is not supported
+ * (RC_ERR_UNSUPPORTED).  N_pad at most 4 194 240 (65 535 x 64).  Cache pointers
+ * 16-byte aligned; kv_scale 4-byte aligned (written by the prefill, read by the
+ * step).  Errors as the bf16 entries. */
 rc_status rc_ref_kv_prefill_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                 const void* q_static, const void* k_static, const void* v_static,
                                 int64_t tok_stride, void* o_static, float* lse_static, void* k_cache8,

@@ -140,8 +140,8 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
       set_error("kv_scale is null");
       return RC_ERR_ARG;
     }
-    if (fp8 && n_pad > (int64_t(1) << 22)) {
-      set_error("FP8 cache of %lld keys per (batch, head) exceeds 2^22", (long long)n_pad);
+    if (fp8 && n_pad > kFp8MaxKeys) {
+      set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_pad, (long long)kFp8MaxKeys);
       return RC_ERR_ARG;
     }
   }
@@ -259,8 +259,8 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
         return RC_ERR_ARG;
       }
       RC_TRY(check_lse(kv_scale, "kv_scale"));
-      if (n_pad > (int64_t(1) << 22)) {
-        set_error("FP8 cache of %lld keys per (batch, head) exceeds 2^22", (long long)n_pad);
+      if (n_pad > kFp8MaxKeys) {
+        set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_pad, (long long)kFp8MaxKeys);
         return RC_ERR_ARG;
       }
     }

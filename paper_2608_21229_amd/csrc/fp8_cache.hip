@@ -10,7 +10,7 @@
 // and code * s is exact in bf16.  Cached segments start at multiples of 16
 // keys; padding keys hold zeros.
 //
-// Four launches on the stream: amax accumulators cleared, per-(b, h) amax
+// Five launches on the stream: amax accumulators cleared, per-(b, h) amax
 // (work-group maxima, then one atomic max per work-group and tensor: the
 // result does not depend on the order), the two quantising stores, and the
 // scales written over the amax values.

@@ -101,6 +101,9 @@ struct CacheStoreParams {
 // H, D]) into K8 [B, H, N_pad, D] and transposed V8 [B, H, D, N_pad]; segment
 // positions in the cache are padded to multiples of kFp8Align keys.
 constexpr int kFp8Align = 16;
+// The transposed-V quantising store runs one work-group row per 64 padded
+// keys (grid y at most 65535).
+constexpr int64_t kFp8MaxKeys = int64_t(65535) * 64;
 struct CacheStore8Params {
   const uint16_t* k_src;
   const uint16_t* v_src;

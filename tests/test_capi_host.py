@@ -293,3 +293,21 @@ def test_fp8_cache_rows_and_errors():
     assert step8(kc=FAKE + 8) == A and pre8(vc=FAKE + 8) == A    # caches need 16-byte alignment
     assert step8(splits=-1) == U
     assert "balanced" in lb.rc_last_error().decode()
+
+
+def test_fp8_cache_key_limit():
+    """The transposed-V store runs one grid row per 64 padded keys: at most 65535 x 64."""
+    lb = rc.lib()
+    for n_ref, want in ((65535 * 64 - 16, rc.RC_OK), (65535 * 64 + 1, rc.RC_ERR_ARG)):
+        L = rc.Layout([(0, 16), (1, 16), (2, 64), (3, n_ref)], "perref")
+        n_pad = L.rows(rc.ROWS_CACHED_FP8)
+        if want == rc.RC_ERR_ARG:
+            assert n_pad > 65535 * 64
+            st = lb.rc_step_masked_attention_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE,
+                                                 FAKE, FAKE, FAKE, None, 1, None, 0, None)
+            assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
+            st = lb.rc_ref_kv_prefill_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE, None,
+                                          FAKE, FAKE, FAKE, None)
+            assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
+        else:
+            assert n_pad == 65535 * 64
