@@ -242,13 +242,13 @@ def fp8_cache(torch, rc, wl, dev, static, live, step_ms_main):
     o8 = torch.empty_like(q_l)
     ob = torch.empty_like(q_l)
     _, _, kc, vc = rc.ref_kv_prefill(L, q_s, k_s, v_s, scale=wl.scale)
-    _, _, k8, v8t, sc = rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, scale=wl.scale)
+    _, _, k8, v8, sc = rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, scale=wl.scale)
     sp = L.auto_splits(B, H, D)
     wsb = L.workspace_bytes(B, H, D, sp)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    pre = time_calls(torch, lambda: rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, o=o_s, k_cache8=k8, v_cache8t=v8t,
+    pre = time_calls(torch, lambda: rc.ref_kv_prefill_fp8(L, q_s, k_s, v_s, o=o_s, k_cache8=k8, v_cache8=v8,
                                                           kv_scale=sc, scale=wl.scale), reps=5)
-    stp = time_calls(torch, lambda: rc.step_masked_attention_fp8(L, q_l, k_l, v_l, k8, v8t, sc, o=o8, splits=sp,
+    stp = time_calls(torch, lambda: rc.step_masked_attention_fp8(L, q_l, k_l, v_l, k8, v8, sc, o=o8, splits=sp,
                                                                  workspace=ws if wsb else None, scale=wl.scale))
     rc.step_masked_attention(L, q_l, k_l, v_l, kc, vc, o=ob, splits=sp, workspace=ws if wsb else None,
                              scale=wl.scale)
@@ -258,10 +258,10 @@ def fp8_cache(torch, rc, wl, dev, static, live, step_ms_main):
     res = {"format": "e4m3fn codes, one power-of-two scale per (batch, head) for K and for V",
            "prefill_ms": pre, "step_ms": stp, "step_tflops": flop / (stp * 1e-3) / 1e12,
            "step_vs_bf16_cache": step_ms_main / stp,
-           "cache_bytes_per_layer": int(k8.numel() + v8t.numel() + 4 * sc.numel()),
+           "cache_bytes_per_layer": int(k8.numel() + v8.numel() + 4 * sc.numel()),
            "bf16_cache_bytes_per_layer": int(2 * (kc.numel() + vc.numel())),
            "output_rel_l2_vs_bf16_cache": rel}
-    del kc, vc, k8, v8t, sc, o_s, o8, ob, ws
+    del kc, vc, k8, v8, sc, o_s, o8, ob, ws
     return res
 
 

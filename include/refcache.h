@@ -101,9 +101,7 @@ typedef enum {
   RC_ROWS_STATIC = 0,  /* tokens of ST and R segments */
   RC_ROWS_LIVE = 1,    /* tokens of LT and X segments */
   RC_ROWS_CACHED = 2,  /* tokens of the cached segments */
-  RC_ROWS_ALL = 3,     /* all tokens */
-  RC_ROWS_CACHED_FP8 = 4  /* key positions of the FP8 cache: each cached segment starts at a
-                             multiple of 16, the total rounded up to 16 (N_pad) */
+  RC_ROWS_ALL = 3      /* all tokens */
 } rc_rows_kind;
 
 typedef struct {
@@ -184,11 +182,8 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
 /* FP8 reference cache (the paper calls caching complementary to other
  * accelerations, Sec. 1 and Sec. 4.2; storing the cache in e4m3 halves its bytes,
  * its residency and the step's cached-key traffic).
- *   k_cache8   [B, H, N_pad, D] e4m3fn codes (bytes), rows in the cache order of
- *              the bf16 cache but each cached segment starting at a multiple of
- *              16 (RC_ROWS_CACHED_FP8 gives N_pad); padding rows hold zeros.
- *   v_cache8t  [B, H, D, N_pad] e4m3fn codes: V transposed (d-major), same key
- *              positions and zero padding.
+ *   k_cache8, v_cache8  [B, H, N_cached, D] e4m3fn codes (bytes), the rows of the
+ *              bf16 cache in the same order.
  *   kv_scale   [B, H, 2] fp32: the scales s_K, s_V of each (batch, head).
  * Quantisation, per (b, h) and tensor X in {K, V} over the cached rows:
  *   amax = max |x|;  s = 2^e with e the smallest integer such that amax / s <= 448
@@ -199,16 +194,16 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
  * bf16 one.  rc_step_masked_attention_fp8 is rc_step_masked_attention with the
  * cached K/V read from the FP8 cache (fresh LT/X K/V stay bf16); splits and
  * workspace as there, except that RC_SPLITS_BALANCED is not supported
- * (RC_ERR_UNSUPPORTED).  N_pad at most 4 194 240 (65 535 x 64).  Cache pointers
+ * (RC_ERR_UNSUPPORTED).  N_cached at most 16 776 960 (65 535 x 256).  Cache pointers
  * 16-byte aligned; kv_scale 4-byte aligned (written by the prefill, read by the
  * step).  Errors as the bf16 entries. */
 rc_status rc_ref_kv_prefill_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                 const void* q_static, const void* k_static, const void* v_static,
                                 int64_t tok_stride, void* o_static, float* lse_static, void* k_cache8,
-                                void* v_cache8t, float* kv_scale, void* stream);
+                                void* v_cache8, float* kv_scale, void* stream);
 rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                        const void* q_live, const void* k_live, const void* v_live,
-                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8t,
+                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8,
                                        const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
                                        void* workspace, size_t ws_bytes, void* stream);
 

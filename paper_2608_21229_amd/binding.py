@@ -20,7 +20,7 @@ RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPA
 SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
 MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE = 0, 1, 2, 3
 ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL = 0, 1, 2
-ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL, ROWS_CACHED_FP8 = 0, 1, 2, 3, 4
+ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL = 0, 1, 2, 3
 MASKS = {"paper": MASK_PAPER, "perref": MASK_PERREF, "isolated": MASK_ISOLATED, "dense": MASK_DENSE}
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librefcache.so")
@@ -312,16 +312,16 @@ def linear(a, w, residual=None, out=None, stream=None):
 
 # ---------------------------------------------------------------- FP8 reference cache
 def fp8_cache_shapes(layout: Layout, B: int, H: int, D: int):
-    """Shapes of the FP8 cache: K8 [B, H, N_pad, D], V8t [B, H, D, N_pad] (uint8
-    e4m3fn codes) and the scales [B, H, 2] (fp32)."""
-    n = layout.rows(ROWS_CACHED_FP8)
-    return (B, H, n, D), (B, H, D, n), (B, H, 2)
+    """Shapes of the FP8 cache: K8 and V8 [B, H, N_cached, D] (uint8 e4m3fn
+    codes, the rows of the bf16 cache) and the scales [B, H, 2] (fp32)."""
+    n = layout.rows(ROWS_CACHED)
+    return (B, H, n, D), (B, H, n, D), (B, H, 2)
 
 
-def ref_kv_prefill_fp8(layout: Layout, q, k, v, o=None, lse=None, k_cache8=None, v_cache8t=None, kv_scale=None,
+def ref_kv_prefill_fp8(layout: Layout, q, k, v, o=None, lse=None, k_cache8=None, v_cache8=None, kv_scale=None,
                        scale: Optional[float] = None, want_lse: bool = False, stream=None):
     """Static-subgraph prefill writing the FP8 cache.  Returns
-    (o, lse or None, k_cache8, v_cache8t, kv_scale)."""
+    (o, lse or None, k_cache8, v_cache8, kv_scale)."""
     torch = _torch()
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
@@ -334,24 +334,24 @@ def ref_kv_prefill_fp8(layout: Layout, q, k, v, o=None, lse=None, k_cache8=None,
         lse = torch.empty((B, H, N), dtype=torch.float32, device=dev)
     if k_cache8 is None:
         k_cache8 = torch.empty(ks, dtype=torch.uint8, device=dev)
-    if v_cache8t is None:
-        v_cache8t = torch.empty(vs, dtype=torch.uint8, device=dev)
+    if v_cache8 is None:
+        v_cache8 = torch.empty(vs, dtype=torch.uint8, device=dev)
     if kv_scale is None:
         kv_scale = torch.empty(ss, dtype=torch.float32, device=dev)
     _expect(o, (B, N, H, D), "torch.bfloat16", "o")
     _expect(lse, (B, H, N), "torch.float32", "lse")
     _expect(k_cache8, ks, "torch.uint8", "k_cache8")
-    _expect(v_cache8t, vs, "torch.uint8", "v_cache8t")
+    _expect(v_cache8, vs, "torch.uint8", "v_cache8")
     _expect(kv_scale, ss, "torch.float32", "kv_scale")
-    _same_device(dev, o=o, lse=lse, k_cache8=k_cache8, v_cache8t=v_cache8t, kv_scale=kv_scale)
+    _same_device(dev, o=o, lse=lse, k_cache8=k_cache8, v_cache8=v_cache8, kv_scale=kv_scale)
     with torch.cuda.device(dev):
         _check(lib().rc_ref_kv_prefill_fp8(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
                                            v.data_ptr(), ts, o.data_ptr(), _ptr(lse), k_cache8.data_ptr(),
-                                           v_cache8t.data_ptr(), kv_scale.data_ptr(), _stream(stream, dev)))
-    return o, lse, k_cache8, v_cache8t, kv_scale
+                                           v_cache8.data_ptr(), kv_scale.data_ptr(), _stream(stream, dev)))
+    return o, lse, k_cache8, v_cache8, kv_scale
 
 
-def step_masked_attention_fp8(layout: Layout, q, k, v, k_cache8, v_cache8t, kv_scale, o=None, lse=None,
+def step_masked_attention_fp8(layout: Layout, q, k, v, k_cache8, v_cache8, kv_scale, o=None, lse=None,
                               splits: int = 0, workspace=None, scale: Optional[float] = None, want_lse: bool = False,
                               stream=None):
     """Per-step attention reading the FP8 cache (fresh LT/X K/V stay bf16).
@@ -369,16 +369,16 @@ def step_masked_attention_fp8(layout: Layout, q, k, v, k_cache8, v_cache8t, kv_s
     _expect(o, (B, N, H, D), "torch.bfloat16", "o")
     _expect(lse, (B, H, N), "torch.float32", "lse")
     _expect(k_cache8, ks, "torch.uint8", "k_cache8")
-    _expect(v_cache8t, vs, "torch.uint8", "v_cache8t")
+    _expect(v_cache8, vs, "torch.uint8", "v_cache8")
     _expect(kv_scale, ss, "torch.float32", "kv_scale")
     need = layout.workspace_bytes(B, H, D, splits) if splits != SPLITS_BALANCED else 0
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
-    _same_device(dev, o=o, lse=lse, k_cache8=k_cache8, v_cache8t=v_cache8t, kv_scale=kv_scale,
+    _same_device(dev, o=o, lse=lse, k_cache8=k_cache8, v_cache8=v_cache8, kv_scale=kv_scale,
                  workspace=workspace if need else None)
     with torch.cuda.device(dev):
         _check(lib().rc_step_masked_attention_fp8(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
-                                                  v.data_ptr(), ts, k_cache8.data_ptr(), v_cache8t.data_ptr(),
+                                                  v.data_ptr(), ts, k_cache8.data_ptr(), v_cache8.data_ptr(),
                                                   kv_scale.data_ptr(), o.data_ptr(), _ptr(lse), splits,
                                                   _ptr(workspace) if need else None, need, _stream(stream, dev)))
     return o, lse

@@ -95,7 +95,7 @@ size_t balanced_workspace_bytes(int32_t D) {
 // A bf16 key source from element strides (batch, head, token) shared by K and V.
 KeySrc bf16_source(const void* k, const void* v, int64_t sb, int64_t sh, int64_t st) {
   return KeySrc{static_cast<const char*>(k), static_cast<const char*>(v), 2 * sb, 2 * sh, 2 * st, 2 * sb, 2 * sh,
-                2 * st, 0};
+                2 * st};
 }
 
 void fill_common(Params& p, int32_t B, int32_t H, float scale) {
@@ -106,7 +106,7 @@ void fill_common(Params& p, int32_t B, int32_t H, float scale) {
   p.lse = nullptr;
   p.ws_o = nullptr;
   p.ws_ml = nullptr;
-  p.src[1] = KeySrc{nullptr, nullptr, 0, 0, 0, 0, 0, 0, 0};
+  p.src[1] = KeySrc{nullptr, nullptr, 0, 0, 0, 0, 0, 0};
 }
 
 }  // namespace
@@ -125,7 +125,6 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   RC_TRY(check_stride(tok_stride, H, D));
   const int64_t n_static = count_rows(L, RowSet::Static);
   const int64_t n_cached = count_cached_rows(L);
-  const int64_t n_pad = count_cached_rows_aligned(L, kFp8Align);
   if (n_static == 0) return RC_OK;  // no ST/R segment: nothing to prefill
   RC_TRY(check_ptr(q_static, "q_static"));
   RC_TRY(check_ptr(k_static, "k_static"));
@@ -134,14 +133,15 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   RC_TRY(check_lse(lse_static, "lse_static"));
   if (n_cached > 0) {
     RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
-    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8t" : "v_cache"));
+    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8" : "v_cache"));
     if (fp8) RC_TRY(check_lse(kv_scale, "kv_scale"));
     if (fp8 && !kv_scale) {
       set_error("kv_scale is null");
       return RC_ERR_ARG;
     }
-    if (fp8 && n_pad > kFp8MaxKeys) {
-      set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_pad, (long long)kFp8MaxKeys);
+    if (fp8 && n_cached > kFp8MaxKeys) {
+      set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_cached,
+                (long long)kFp8MaxKeys);
       return RC_ERR_ARG;
     }
   }
@@ -160,7 +160,7 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   p.src[0] = bf16_source(k_static, v_static, tok_stride * n_static, D, tok_stride);
 
   // the cached segments' rows inside the static buffers and their cache
-  // positions (padded to multiples of kFp8Align in the FP8 cache)
+  // positions
   CopySeg seg[RC_MAX_SEGMENTS];
   int n_copy = 0;
   {
@@ -169,7 +169,6 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
     for (int i = 0; i < L->n_seg; ++i) {
       if (!is_static_kind(L->seg[i].kind)) continue;
       if (cm >> i & 1u) {
-        if (fp8) drow = (drow + kFp8Align - 1) / kFp8Align * kFp8Align;
         seg[n_copy++] = CopySeg{srow, L->seg[i].len, drow};
         drow += L->seg[i].len;
       }
@@ -205,27 +204,27 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   c.k_src = static_cast<const uint16_t*>(k_static);
   c.v_src = static_cast<const uint16_t*>(v_static);
   c.k_dst = static_cast<uint8_t*>(k_cache);
-  c.vt_dst = static_cast<uint8_t*>(v_cache);
+  c.v_dst = static_cast<uint8_t*>(v_cache);
   c.kv_scale = kv_scale;
   c.src_st = tok_stride;
   c.src_sb = tok_stride * n_static;
   c.B = B;
   c.H = H;
   c.D = D;
-  c.n_pad = int32_t(n_pad);
+  c.n_cached = int32_t(n_cached);
   c.n_copy = n_copy;
   for (int i = 0; i < n_copy; ++i) c.seg[i] = seg[i];
-  c.total_rows = int32_t(n_cached);
-  // the quantising store's grids: (B H) x padded-row blocks, one thread per K8 granule
+  // the quantising store's grids: (B H) x row blocks (amax), one thread per
+  // 16-byte granule of K and of V
   RC_TRY(check_blocks(int64_t(B) * H, "FP8 cache store"));
-  RC_TRY(check_blocks((int64_t(B) * H * n_pad * (D / 8) + 255) / 256, "FP8 cache store"));
+  RC_TRY(check_blocks((int64_t(B) * H * n_cached * (D / 8) + 255) / 256, "FP8 cache store"));
   RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
   if (n_cached > 0) RC_TRY(hip_status(launch_cache_store_fp8(c, stream), "FP8 cache store launch"));
   return RC_OK;
 }
 
-// The per-step attention over either cache format (bf16, or FP8: K8 and the
-// transposed V8 with their scales).
+// The per-step attention over either cache format (bf16, or FP8: K8 and V8
+// with their scales).
 rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q_live,
                     const void* k_live, const void* v_live, int64_t tok_stride, bool fp8, const void* k_cache,
                     const void* v_cache, const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
@@ -239,7 +238,6 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   }
   const int64_t n_live = count_rows(L, RowSet::Live);
   const int64_t n_cached = count_cached_rows(L);
-  const int64_t n_pad = count_cached_rows_aligned(L, kFp8Align);
   if (fp8 && splits == kSplitsBalanced) {
     set_error("the balanced schedule is not available with the FP8 cache");
     return RC_ERR_UNSUPPORTED;
@@ -252,15 +250,16 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   RC_TRY(check_lse(lse_live, "lse_live"));
   if (n_cached > 0) {
     RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
-    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8t" : "v_cache"));
+    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8" : "v_cache"));
     if (fp8) {
       if (!kv_scale) {
         set_error("kv_scale is null");
         return RC_ERR_ARG;
       }
       RC_TRY(check_lse(kv_scale, "kv_scale"));
-      if (n_pad > kFp8MaxKeys) {
-        set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_pad, (long long)kFp8MaxKeys);
+      if (n_cached > kFp8MaxKeys) {
+        set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_cached,
+                  (long long)kFp8MaxKeys);
         return RC_ERR_ARG;
       }
     }
@@ -268,9 +267,8 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
-  RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8 ? kFp8Align : 1));
-  // the automatic choice is the one rc_step_auto_splits reports (from the
-  // unpadded plan, which the FP8 padding can change by a few key tiles)
+  RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
+  // the automatic choice is the one rc_step_auto_splits reports
   if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
   p.splits = splits;
   const bool balanced = p.splits == kSplitsBalanced;
@@ -291,8 +289,8 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   if (fp8) {
     p.fp8 = 1;
     p.kv_scale = kv_scale;
-    p.src[1] = KeySrc{static_cast<const char*>(k_cache), static_cast<const char*>(v_cache), int64_t(H) * n_pad * D,
-                      n_pad * D, D, int64_t(H) * D * n_pad, D * n_pad, 1, n_pad};
+    p.src[1] = KeySrc{static_cast<const char*>(k_cache), static_cast<const char*>(v_cache), int64_t(H) * n_cached * D,
+                      n_cached * D, D, int64_t(H) * n_cached * D, n_cached * D, D};
   } else {
     p.src[1] = bf16_source(k_cache, v_cache, int64_t(H) * n_cached * D, n_cached * D, D);
   }
@@ -358,9 +356,9 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
 rc_status rc_ref_kv_prefill_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                 const void* q_static, const void* k_static, const void* v_static,
                                 int64_t tok_stride, void* o_static, float* lse_static, void* k_cache8,
-                                void* v_cache8t, float* kv_scale, void* stream) {
+                                void* v_cache8, float* kv_scale, void* stream) {
   return prefill_impl(L, B, H, D, scale, q_static, k_static, v_static, tok_stride, o_static, lse_static, true,
-                      k_cache8, v_cache8t, kv_scale, stream);
+                      k_cache8, v_cache8, kv_scale, stream);
 }
 
 int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D) {
@@ -395,10 +393,10 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
 
 rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                        const void* q_live, const void* k_live, const void* v_live,
-                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8t,
+                                       int64_t tok_stride, const void* k_cache8, const void* v_cache8,
                                        const float* kv_scale, void* o_live, float* lse_live, int32_t splits,
                                        void* workspace, size_t ws_bytes, void* stream) {
-  return step_impl(L, B, H, D, scale, q_live, k_live, v_live, tok_stride, true, k_cache8, v_cache8t, kv_scale,
+  return step_impl(L, B, H, D, scale, q_live, k_live, v_live, tok_stride, true, k_cache8, v_cache8, kv_scale,
                    o_live, lse_live, splits, workspace, ws_bytes, stream);
 }
 

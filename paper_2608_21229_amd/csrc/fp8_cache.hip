@@ -1,19 +1,19 @@
 // FP8 (e4m3fn) reference cache store: quantise the cached segments' K/V rows
-// of the static buffers into K8 [B, H, N_pad, D] and transposed V8 [B, H, D,
-// N_pad] with one power-of-two scale per (batch, head) and tensor.
+// of the static buffers into K8 and V8 [B, H, N_cached, D] (the rows of the
+// bf16 cache, one byte per value) with one power-of-two scale per (batch,
+// head) and tensor.
 //
 // Per (b, h) and tensor X: amax = max |x| over the cached rows; the scale is
 // s = 2^e with e the smallest integer such that amax / s <= 448 (the largest
 // finite e4m3fn value), s = 1 when amax = 0; the code of x is the nearest
 // e4m3fn value of x / s (ties to even), which the hardware conversion
 // computes.  Dividing by a power of two is exact, so a code depends on x alone,
-// and code * s is exact in bf16.  Cached segments start at multiples of 16
-// keys; padding keys hold zeros.
+// and code * s is exact in bf16.
 //
 // Five launches on the stream: amax accumulators cleared, per-(b, h) amax
 // (work-group maxima, then one atomic max per work-group and tensor: the
-// result does not depend on the order), the two quantising stores, and the
-// scales written over the amax values.
+// result does not depend on the order), the quantising stores of K and of V,
+// and the scales written over the amax values.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -36,13 +36,11 @@ __device__ __forceinline__ int fp8_exponent(float amax) {
   return m <= 0.875f ? k - 9 : k - 8;
 }
 
-// Source row of padded cache position pos, or -1 for a padding position.
+// Source row (in the static buffers) of cache position pos.
 __device__ __forceinline__ int source_row(const CacheStore8Params& c, int pos) {
-  for (int i = 0; i < c.n_copy; ++i) {
-    const CopySeg& sg = c.seg[i];
-    if (pos >= sg.dst_row0 && pos < sg.dst_row0 + sg.len) return sg.src_row0 + (pos - sg.dst_row0);
-  }
-  return -1;
+  int i = 0;
+  while (i + 1 < c.n_copy && pos >= c.seg[i + 1].dst_row0) ++i;
+  return c.seg[i].src_row0 + (pos - c.seg[i].dst_row0);
 }
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
@@ -78,7 +76,7 @@ __global__ void fill_zero_kernel(float* a, int n) {
   if (i < n) a[i] = 0.f;
 }
 
-// Grid (B * H, ceil(n_pad / kRowsPerBlock)); 256 threads stride over the
+// Grid (B * H, ceil(n_cached / kRowsPerBlock)); 256 threads stride over the
 // block's rows x D/8 granules of K and V.
 __global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
   const int bh = blockIdx.x, b = bh / c.H, h = bh % c.H;
@@ -87,9 +85,8 @@ __global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
   float mk = 0.f, mv = 0.f;
   for (int g = threadIdx.x; g < kRowsPerBlock * gr; g += blockDim.x) {
     const int pos = row0 + g / gr;
-    if (pos >= c.n_pad) break;
+    if (pos >= c.n_cached) break;
     const int srow = source_row(c, pos);
-    if (srow < 0) continue;
     const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + (g % gr) * 8;
     mk = fmaxf(mk, amax8(*reinterpret_cast<const u32x4*>(c.k_src + off)));
     mv = fmaxf(mv, amax8(*reinterpret_cast<const u32x4*>(c.v_src + off)));
@@ -112,62 +109,24 @@ __global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
   }
 }
 
-// K8: one thread per (b, h, padded row, granule of 8 elements).
-__global__ __launch_bounds__(256) void quant_k_kernel(const CacheStore8Params c) {
+// K8 or V8 (`which` 0 or 1): one thread per (b, h, cached row, granule of 8
+// elements).
+__global__ __launch_bounds__(256) void quant_kernel(const CacheStore8Params c, int which) {
   const int gr = c.D / 8;
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t total = int64_t(c.B) * c.H * c.n_pad * gr;
+  const int64_t total = int64_t(c.B) * c.H * c.n_cached * gr;
   if (idx >= total) return;
   const int g = int(idx % gr);
   int64_t rest = idx / gr;
-  const int pos = int(rest % c.n_pad);
-  const int64_t bh = rest / c.n_pad;
+  const int pos = int(rest % c.n_cached);
+  const int64_t bh = rest / c.n_cached;
   const int b = int(bh / c.H), h = int(bh % c.H);
   const int srow = source_row(c, pos);
-  u32x2 q = {0u, 0u};
-  if (srow >= 0) {
-    const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
-    q = quant8(*reinterpret_cast<const u32x4*>(c.k_src + off), fp8_exponent(c.kv_scale[bh * 2]));
-  }
-  *reinterpret_cast<u32x2*>(c.k_dst + (bh * c.n_pad + pos) * c.D + g * 8) = q;
-}
-
-// V8t: one work-group per (b, h, 64 padded positions): quantise the 64 x D
-// block into LDS as [key][d] codes, then write D rows of 64 (or fewer, at the
-// end) key codes with 16-byte stores.
-__global__ __launch_bounds__(256) void quant_vt_kernel(const CacheStore8Params c) {
-  __shared__ uint8_t tile[64 * 128];
-  const int bh = blockIdx.x, b = bh / c.H, h = bh % c.H;
-  const int pos0 = blockIdx.y * 64;
-  const int gr = c.D / 8;
-  const int e = fp8_exponent(c.kv_scale[bh * 2 + 1]);
-  for (int g = threadIdx.x; g < 64 * gr; g += blockDim.x) {
-    const int key = g / gr, gi = g % gr;
-    const int pos = pos0 + key;
-    const int srow = pos < c.n_pad ? source_row(c, pos) : -1;
-    u32x2 q = {0u, 0u};
-    if (srow >= 0) {
-      const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + gi * 8;
-      q = quant8(*reinterpret_cast<const u32x4*>(c.v_src + off), e);
-    }
-    *reinterpret_cast<u32x2*>(tile + key * c.D + gi * 8) = q;
-  }
-  __syncthreads();
-  const int nkeys = min(64, c.n_pad - pos0);  // a multiple of 16
-  for (int w = threadIdx.x; w < c.D * 4; w += blockDim.x) {
-    const int d = w / 4, kg = w % 4;
-    if (kg * 16 >= nkeys) continue;
-    uint32_t word[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      uint32_t x = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) x |= uint32_t(tile[(kg * 16 + 4 * j + i) * c.D + d]) << (8 * i);
-      word[j] = x;
-    }
-    *reinterpret_cast<u32x4*>(c.vt_dst + (int64_t(bh) * c.D + d) * c.n_pad + pos0 + kg * 16) =
-        u32x4{word[0], word[1], word[2], word[3]};
-  }
+  const uint16_t* src = which ? c.v_src : c.k_src;
+  uint8_t* dst = which ? c.v_dst : c.k_dst;
+  const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
+  const u32x2 q = quant8(*reinterpret_cast<const u32x4*>(src + off), fp8_exponent(c.kv_scale[bh * 2 + which]));
+  *reinterpret_cast<u32x2*>(dst + (bh * c.n_cached + pos) * c.D + g * 8) = q;
 }
 
 __global__ void finalize_scale_kernel(float* a, int n) {
@@ -180,12 +139,13 @@ __global__ void finalize_scale_kernel(float* a, int n) {
 int launch_cache_store_fp8(const CacheStore8Params& c, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nsc = c.B * c.H * 2;
-  if (nsc == 0 || c.n_pad == 0) return 0;
+  if (nsc == 0 || c.n_cached == 0) return 0;
   hipLaunchKernelGGL(fill_zero_kernel, dim3((nsc + 255) / 256), dim3(256), 0, s, c.kv_scale, nsc);
-  hipLaunchKernelGGL(amax_kernel, dim3(c.B * c.H, (c.n_pad + kRowsPerBlock - 1) / kRowsPerBlock), dim3(256), 0, s, c);
-  const int64_t tk = int64_t(c.B) * c.H * c.n_pad * (c.D / 8);
-  hipLaunchKernelGGL(quant_k_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c);
-  hipLaunchKernelGGL(quant_vt_kernel, dim3(c.B * c.H, (c.n_pad + 63) / 64), dim3(256), 0, s, c);
+  hipLaunchKernelGGL(amax_kernel, dim3(c.B * c.H, (c.n_cached + kRowsPerBlock - 1) / kRowsPerBlock), dim3(256), 0, s,
+                     c);
+  const int64_t tk = int64_t(c.B) * c.H * c.n_cached * (c.D / 8);
+  hipLaunchKernelGGL(quant_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c, 0);
+  hipLaunchKernelGGL(quant_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c, 1);
   hipLaunchKernelGGL(finalize_scale_kernel, dim3((nsc + 255) / 256), dim3(256), 0, s, c.kv_scale, nsc);
   return int(hipGetLastError());
 }

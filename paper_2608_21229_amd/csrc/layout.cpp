@@ -118,19 +118,11 @@ int64_t count_cached_rows(const rc_layout* L) {
   return n;
 }
 
-int64_t count_cached_rows_aligned(const rc_layout* L, int align) {
-  const uint32_t m = cached_mask(L);
-  int64_t n = 0;
-  for (int i = 0; i < L->n_seg; ++i)
-    if (m >> i & 1u) n = (n + align - 1) / align * align + L->seg[i].len;
-  return (n + align - 1) / align * align;
-}
-
 static RowSet rows_of(int32_t entry) {
   return entry == RC_ENTRY_PREFILL ? RowSet::Static : entry == RC_ENTRY_STEP ? RowSet::Live : RowSet::All;
 }
 
-rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align) {
+rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first) {
   const RowSet rset = rows_of(entry);
   // Position of every segment inside each key source.
   int32_t src_of[RC_MAX_SEGMENTS], pos_of[RC_MAX_SEGMENTS], row_of[RC_MAX_SEGMENTS];
@@ -151,7 +143,6 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align) {
       pos_entry += L->seg[i].len;
     } else if (entry == RC_ENTRY_STEP && (cmask >> i & 1u)) {
       src_of[i] = 1;
-      pos_cache = (pos_cache + cache_align - 1) / cache_align * cache_align;
       pos_of[i] = pos_cache;
       pos_cache += L->seg[i].len;
     }
@@ -181,7 +172,7 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align) {
         ++nr;
       }
     }
-    if (cache_align > 1) {
+    if (fresh_first) {
       // FP8 cache: fresh (bf16) ranges first, then cache ranges, so that the
       // kernel runs one ring over each tile kind (softmax is order-free)
       KeyRange part[RC_MAX_SEGMENTS];
@@ -319,7 +310,6 @@ int64_t rc_rows(const rc_layout* L, int32_t which) {
     case RC_ROWS_STATIC: return rc::count_rows(L, rc::RowSet::Static);
     case RC_ROWS_LIVE: return rc::count_rows(L, rc::RowSet::Live);
     case RC_ROWS_CACHED: return rc::count_cached_rows(L);
-    case RC_ROWS_CACHED_FP8: return rc::count_cached_rows_aligned(L, rc::kFp8Align);
     case RC_ROWS_ALL: return rc::count_rows(L, rc::RowSet::All);
     default:
       rc::set_error("unknown row class %d", which);

@@ -51,15 +51,13 @@ struct QSeg {
 };
 
 // A key source, addressed in bytes.  bf16 sources hold K and V as
-// [B, N, H, D] with one token stride; the FP8 cache holds K as
-// [B, H, N_pad, D] bytes and V transposed as [B, H, D, N_pad] bytes (token
-// stride 1, d rows v_row = N_pad bytes apart).
+// [B, N, H, D] with one token stride; the FP8 cache holds K8 and V8 as
+// [B, H, N_cached, D] bytes.
 struct KeySrc {
   const char* k;
   const char* v;
   int64_t k_sb, k_sh, k_st;  // byte strides of K: batch, head, token
   int64_t v_sb, v_sh, v_st;  // byte strides of V: batch, head, token
-  int64_t v_row;             // transposed FP8 V: bytes between d rows; 0 otherwise
 };
 
 struct Params {
@@ -98,21 +96,20 @@ struct CacheStoreParams {
 };
 
 // FP8 cache store: quantise the cached segments' K/V rows (bf16, [B, N_static,
-// H, D]) into K8 [B, H, N_pad, D] and transposed V8 [B, H, D, N_pad]; segment
-// positions in the cache are padded to multiples of kFp8Align keys.
-constexpr int kFp8Align = 16;
-// The transposed-V quantising store runs one work-group row per 64 padded
-// keys (grid y at most 65535).
-constexpr int64_t kFp8MaxKeys = int64_t(65535) * 64;
+// H, D]) into K8 and V8 [B, H, N_cached, D] (the bf16 cache's rows, one byte
+// per value).
+// The amax pass runs one work-group row per 256 cached keys (grid y at most
+// 65535).
+constexpr int64_t kFp8MaxKeys = int64_t(65535) * 256;
 struct CacheStore8Params {
   const uint16_t* k_src;
   const uint16_t* v_src;
   uint8_t* k_dst;
-  uint8_t* vt_dst;
+  uint8_t* v_dst;
   float* kv_scale;     // [B, H, 2]: amax while quantising, the scales afterwards
   int64_t src_sb, src_st;
-  int32_t B, H, D, n_pad, n_copy, total_rows;
-  CopySeg seg[RC_MAX_SEGMENTS];  // dst_row0: padded position
+  int32_t B, H, D, n_cached, n_copy;
+  CopySeg seg[RC_MAX_SEGMENTS];
 };
 
 // Dense projection out = A W^T (+ R) of the chained synthetic layer.
@@ -143,9 +140,8 @@ rc_status check_layout(const rc_layout* L, int32_t entry);  // sets the thread e
 uint32_t cached_mask(const rc_layout* L);                  // bit i: segment i is cached
 int64_t count_rows(const rc_layout* L, RowSet set);
 int64_t count_cached_rows(const rc_layout* L);
-int64_t count_cached_rows_aligned(const rc_layout* L, int align);  // padded cache length
 // Fill p.qseg / p.range / n_qseg / n_qtiles / n_rows for an entry.
-rc_status plan(const rc_layout* L, int32_t entry, Params& p, int cache_align = 1);
+rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first = false);
 int32_t auto_splits(const Params& p);
 
 void set_error(const char* fmt, ...);

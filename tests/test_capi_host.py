@@ -269,11 +269,10 @@ def test_linear_binding_rejects_host_tensors():
 
 
 def test_fp8_cache_rows_and_errors():
-    # cached segments start at multiples of 16: ST 5 -> [0, 5), R 33 -> [16, 49), R 7 -> [64, 71); N_pad 80
+    # the FP8 cache holds the bf16 cache's rows: ST 5 + R 33 + R 7
     L = rc.Layout([(0, 5), (1, 8), (2, 16), (3, 33), (3, 7)], "perref")
     assert L.rows(rc.ROWS_CACHED) == 45
-    assert L.rows(rc.ROWS_CACHED_FP8) == 80
-    assert rc.fp8_cache_shapes(L, 2, 3, 64) == ((2, 3, 80, 64), (2, 3, 64, 80), (2, 3, 2))
+    assert rc.fp8_cache_shapes(L, 2, 3, 64) == ((2, 3, 45, 64), (2, 3, 45, 64), (2, 3, 2))
     lb = rc.lib()
     A, U = rc.RC_ERR_ARG, rc.RC_ERR_UNSUPPORTED
     args = lambda **kw: dict(dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, kc=FAKE, vc=FAKE, sc=FAKE, splits=1), **kw)
@@ -296,18 +295,18 @@ def test_fp8_cache_rows_and_errors():
 
 
 def test_fp8_cache_key_limit():
-    """The transposed-V store runs one grid row per 64 padded keys: at most 65535 x 64."""
+    """The amax pass runs one grid row per 256 cached keys: at most 65535 x 256."""
     lb = rc.lib()
-    for n_ref, want in ((65535 * 64 - 16, rc.RC_OK), (65535 * 64 + 1, rc.RC_ERR_ARG)):
+    lim = 65535 * 256
+    for n_ref, ok in ((lim - 16, True), (lim - 15, False)):
         L = rc.Layout([(0, 16), (1, 16), (2, 64), (3, n_ref)], "perref")
-        n_pad = L.rows(rc.ROWS_CACHED_FP8)
-        if want == rc.RC_ERR_ARG:
-            assert n_pad > 65535 * 64
-            st = lb.rc_step_masked_attention_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE,
-                                                 FAKE, FAKE, FAKE, None, 1, None, 0, None)
-            assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
-            st = lb.rc_ref_kv_prefill_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE, None,
-                                          FAKE, FAKE, FAKE, None)
-            assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
-        else:
-            assert n_pad == 65535 * 64
+        n_cached = L.rows(rc.ROWS_CACHED)
+        assert (n_cached <= lim) == ok
+        if ok:
+            continue
+        st = lb.rc_step_masked_attention_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE,
+                                             FAKE, FAKE, FAKE, None, 1, None, 0, None)
+        assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
+        st = lb.rc_ref_kv_prefill_fp8(ctypes.byref(L.c), 1, 2, 64, 0.125, FAKE, FAKE, FAKE, 128, FAKE, None,
+                                      FAKE, FAKE, FAKE, None)
+        assert st == rc.RC_ERR_ARG and "exceeds" in lb.rc_last_error().decode()
