@@ -106,10 +106,10 @@ def cpu_baseline(wl, mask: str, threads_hint: int):
     oa.denoise_step(kinds, lens, vis, ql, kl, vl, kc, vc, wl.scale, rows=rows)
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    # one thread, on every 32nd live row (about the same seconds as the whole
-    # step on all cores of a 16-core host)
+    # one thread, on every 8th live row (a few seconds: the whole sample stays
+    # at about 10-15 s of CPU time on a 16-core host)
     from threadpoolctl import threadpool_limits
-    rows1 = np.arange(0, n_live, 32)
+    rows1 = np.arange(0, n_live, 8)
     flops1 = 4.0 * D * H * B * float(keys_per_row[rows1].sum())
     with threadpool_limits(limits=1):
         t1 = time.perf_counter()
@@ -135,7 +135,7 @@ def cpu_baseline(wl, mask: str, threads_hint: int):
         "host_cpus": os.cpu_count(),
         "cpu_model": cpu_model,
         "one_thread": {"value": flops1 / dt1 / 1e12, "seconds": dt1,
-                       "sample": f"every 32nd live row ({len(rows1)} rows) x {H} heads, 1 BLAS thread"},
+                       "sample": f"every 8th live row ({len(rows1)} rows) x {H} heads, 1 BLAS thread"},
     }
 
 
