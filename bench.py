@@ -31,7 +31,6 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-STEP_KERNEL = "attn_fwd_kernel<128, false, false>"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_21229_amd", "csrc", "attn_fwd.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_fwd_ref5_step_traffic.txt")
 PAPER_CONTEXT = {
@@ -333,6 +332,9 @@ def main():
     ap.add_argument("--no-full", action="store_true", help="skip the dense full-recompute comparison")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the side measurements (anchor overhead, one GPU's head share, CFG batch)")
+    ap.add_argument("--fp8-cache", action="store_true",
+                    help="store the reference cache as e4m3 codes (rc_ref_kv_prefill_fp8 / "
+                         "rc_step_masked_attention_fp8) instead of bf16; compute stays bf16")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (reference for rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -377,8 +379,13 @@ def main():
         static.append([gen_bf16(torch, (B, n_static, H, D), gen, wl.std, dev) for _ in range(3)])
         live.append([[gen_bf16(torch, (B, n_live, H, D), gen, wl.std, dev) for _ in range(3)]
                      for _ in range(n_live_sets)])
-        caches.append((torch.empty((B, H, n_cached, D), dtype=torch.bfloat16, device=dev),
-                       torch.empty((B, H, n_cached, D), dtype=torch.bfloat16, device=dev)))
+        if args.fp8_cache:
+            caches.append((torch.empty((B, H, n_cached, D), dtype=torch.uint8, device=dev),
+                           torch.empty((B, H, n_cached, D), dtype=torch.uint8, device=dev),
+                           torch.empty((B, H, 2), dtype=torch.float32, device=dev)))
+        else:
+            caches.append((torch.empty((B, H, n_cached, D), dtype=torch.bfloat16, device=dev),
+                           torch.empty((B, H, n_cached, D), dtype=torch.bfloat16, device=dev)))
     o_static = torch.empty((B, n_static, H, D), dtype=torch.bfloat16, device=dev)
     o_live = torch.empty((B, n_live, H, D), dtype=torch.bfloat16, device=dev)
     ws_bytes = L.workspace_bytes(B, H, D, splits)
@@ -396,8 +403,12 @@ def main():
             q, k, v = static[layer]
             if it is not None:
                 ev_pre[it][layer][0].record()
-            rc.ref_kv_prefill(L, q, k, v, o=o_static, k_cache=caches[layer][0], v_cache=caches[layer][1],
-                              scale=wl.scale)
+            if args.fp8_cache:
+                rc.ref_kv_prefill_fp8(L, q, k, v, o=o_static, k_cache8=caches[layer][0], v_cache8=caches[layer][1],
+                                      kv_scale=caches[layer][2], scale=wl.scale)
+            else:
+                rc.ref_kv_prefill(L, q, k, v, o=o_static, k_cache=caches[layer][0], v_cache=caches[layer][1],
+                                  scale=wl.scale)
             if it is not None:
                 ev_pre[it][layer][1].record()
         i = 0
@@ -406,8 +417,12 @@ def main():
                 q, k, v = live[layer][s % n_live_sets]
                 if it is not None:
                     ev[it][i][0].record()
-                rc.step_masked_attention(L, q, k, v, caches[layer][0], caches[layer][1], o=o_live, splits=splits,
-                                         workspace=ws if ws_bytes else None, scale=wl.scale)
+                if args.fp8_cache:
+                    rc.step_masked_attention_fp8(L, q, k, v, *caches[layer], o=o_live, splits=splits,
+                                                 workspace=ws if ws_bytes else None, scale=wl.scale)
+                else:
+                    rc.step_masked_attention(L, q, k, v, caches[layer][0], caches[layer][1], o=o_live,
+                                             splits=splits, workspace=ws if ws_bytes else None, scale=wl.scale)
                 if it is not None:
                     ev[it][i][1].record()
                 i += 1
@@ -462,10 +477,13 @@ def main():
         del q, k, v, ob
 
     side = None
-    if not args.no_extras and LAYERS == 1 and B == 1:
+    if not args.no_extras and not args.fp8_cache and LAYERS == 1 and B == 1:
         side = extras(torch, rc, wl, gen, dev, static[0], live[0][0], step_avg)
 
-    traffic = measured_traffic(args.config) if splits == 1 else None
+    # the committed counter summary covers the bf16-cache step kernel
+    traffic = measured_traffic(args.config) if splits == 1 and not args.fp8_cache else None
+    f8 = "true" if args.fp8_cache else "false"
+    cached_bytes = 1 if args.fp8_cache else 2
     out = {
         "metric": "useful masked-attention TFLOP/s (% of bf16 MFMA peak; per-step ms at 5 refs)",
         "value": value,
@@ -486,6 +504,7 @@ def main():
             "layers": LAYERS,
             "denoise_steps": T,
             "split_kv": splits,
+            "cache": "e4m3 codes + per-(batch, head) scales" if args.fp8_cache else "bf16",
             "useful_tflop_per_request": flop_request / 1e12,
         },
         "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
@@ -496,14 +515,15 @@ def main():
         "prefill_ms": pre_avg,
         "prefill_tflops": flop_pre / (pre_avg * 1e-3) / 1e12,
         "roofline": {
-            "kernel": STEP_KERNEL if splits == 1 else "attn_fwd_kernel<128, true> + combine_kernel",
+            "kernel": (f"attn_fwd_kernel<128, false, {f8}>" if splits == 1
+                       else f"attn_fwd_kernel<128, true, {f8}> + combine_kernel"),
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": traffic,
-            "algorithmic_bytes_per_launch": 2.0 * B * H * D * (4 * n_live + 2 * n_cached),
+            "algorithmic_bytes_per_launch": 2.0 * B * H * D * (4 * n_live + cached_bytes * n_cached),
             "useful_flop_per_launch": flop_step,
         },
         "full_recompute": full,
