@@ -307,7 +307,13 @@ def chained_layers(torch, rc, wl, dev, layers=4, steps=40):
     hb = h0[:, n_st:]
     assert hb.shape[1] == Lb.rows(rc.ROWS_ALL)
     base = time_calls(torch, lambda: ch_base.full(hb), reps=3, warm=1)
+    # the same chain over the FP8 reference cache
+    ch8 = rc.Chain(L, ch.w_qkv, ch.w_o, H, D, cache="fp8")
+    caches8 = ch8.prefill(h_s)
+    pre8 = time_calls(torch, lambda: ch8.prefill(h_s, caches=caches8), reps=3, warm=1)
+    stp8 = time_calls(torch, lambda: ch8.step(h_l, caches8), reps=10)
     res = {"layers": layers, "mask": "perref", "hidden": C,
+           "fp8_cache_prefill_ms": pre8, "fp8_cache_step_ms": stp8,
            "dense_base_ms": base, "speedup_per_step_vs_dense_base": base / stp,
            f"speedup_request_{steps}_steps_vs_dense_base": steps * base / (pre + steps * stp),
            "prefill_ms": pre, "step_ms": stp, "full_recompute_ms": full,
@@ -316,7 +322,7 @@ def chained_layers(torch, rc, wl, dev, layers=4, steps=40):
            "step_tflops": step_flop / (stp * 1e-3) / 1e12, "full_recompute_tflops": full_flop / (full * 1e-3) / 1e12,
            "speedup_per_step": full / stp,
            f"speedup_request_{steps}_steps": steps * full / (pre + steps * stp)}
-    del ch, ch_base, caches, h_s, h_l, h0, hb, qkv, hw, o
+    del ch, ch_base, ch8, caches, caches8, h_s, h_l, h0, hb, qkv, hw, o
     return res
 
 

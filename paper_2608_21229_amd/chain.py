@@ -16,6 +16,10 @@ Three ways through the stack:
     full     every row through every layer: the recompute baseline, in which
              every token is re-projected and attended at each step
 
+With ``cache="fp8"`` each layer's reference cache is stored as e4m3 codes
+with per-(batch, head) scales (``ref_kv_prefill_fp8`` /
+``step_masked_attention_fp8``); the computation stays bf16.
+
 Marshalling only: every multiply-add runs in librefcache.  Work buffers come
 from torch's allocator; ``collect`` (a list) receives a copy of the hidden
 state after each layer.
@@ -34,9 +38,12 @@ class Chain:
     w_qkv[l]: [3 H D, H D] bf16, w_o[l]: [H D, H D] bf16, on one GPU."""
 
     def __init__(self, layout: rcb.Layout, w_qkv: Sequence, w_o: Sequence, H: int, D: int,
-                 scale: Optional[float] = None):
+                 scale: Optional[float] = None, cache: str = "bf16"):
         if len(w_qkv) != len(w_o) or not w_qkv:
             raise ValueError("need one W_qkv and one W_o per layer")
+        if cache not in ("bf16", "fp8"):
+            raise ValueError(f"cache must be 'bf16' or 'fp8', got {cache!r}")
+        self.cache = cache
         C = H * D
         for l, (wq, wo) in enumerate(zip(w_qkv, w_o)):
             if tuple(wq.shape) != (3 * C, C) or tuple(wo.shape) != (C, C):
@@ -82,7 +89,13 @@ class Chain:
         return src.view(B, N, self.C)
 
     def new_caches(self, B: int, device) -> List[Tuple]:
+        """Per layer (K_cache, V_cache) bf16, or (K8, V8, scales) for the FP8 cache."""
         torch = rcb._torch()
+        if self.cache == "fp8":
+            ks, vs, ss = rcb.fp8_cache_shapes(self.layout, B, self.H, self.D)
+            return [(torch.empty(ks, dtype=torch.uint8, device=device),
+                     torch.empty(vs, dtype=torch.uint8, device=device),
+                     torch.empty(ss, dtype=torch.float32, device=device)) for _ in range(self.layers)]
         nc = self.layout.rows(rcb.ROWS_CACHED)
         shape = (B, self.H, nc, self.D)
         return [(torch.empty(shape, dtype=torch.bfloat16, device=device),
@@ -90,16 +103,20 @@ class Chain:
 
     def prefill(self, h_static, caches=None, collect: Optional[List] = None, stream=None):
         """h_static [B, N_static, H D]: the ST and R rows in sequence order.
-        Fills and returns one (K_cache, V_cache) pair per layer.  The static
+        Fills and returns one cache entry per layer (see ``new_caches``).  The static
         rows' output projection of the last layer is skipped (nobody reads
         it) unless ``collect`` asks for the hidden states."""
         caches = self.new_caches(h_static.shape[0], h_static.device) if caches is None else caches
         if len(caches) != self.layers:
-            raise ValueError(f"need {self.layers} cache pairs, got {len(caches)}")
+            raise ValueError(f"need {self.layers} cache entries, got {len(caches)}")
 
         def attend(l, q, k, v, o):
-            rcb.ref_kv_prefill(self.layout, q, k, v, o=o, k_cache=caches[l][0], v_cache=caches[l][1],
-                               scale=self.scale, stream=stream)
+            if self.cache == "fp8":
+                rcb.ref_kv_prefill_fp8(self.layout, q, k, v, o=o, k_cache8=caches[l][0], v_cache8=caches[l][1],
+                                       kv_scale=caches[l][2], scale=self.scale, stream=stream)
+            else:
+                rcb.ref_kv_prefill(self.layout, q, k, v, o=o, k_cache=caches[l][0], v_cache=caches[l][1],
+                                   scale=self.scale, stream=stream)
 
         self._run(h_static, rcb.ROWS_STATIC, attend, collect, last_out=False, stream=stream)
         return caches
@@ -108,15 +125,19 @@ class Chain:
         """h_live [B, N_live, H D]: the LT and X rows of one denoising step.
         Returns the live rows' hidden state after the last layer."""
         if len(caches) != self.layers:
-            raise ValueError(f"need {self.layers} cache pairs, got {len(caches)}")
+            raise ValueError(f"need {self.layers} cache entries, got {len(caches)}")
         torch = rcb._torch()
         B = h_live.shape[0]
         need = self.layout.workspace_bytes(B, self.H, self.D, splits)
         ws = torch.empty(need, dtype=torch.uint8, device=h_live.device) if need else None
 
         def attend(l, q, k, v, o):
-            rcb.step_masked_attention(self.layout, q, k, v, caches[l][0], caches[l][1], o=o, splits=splits,
-                                      workspace=ws, scale=self.scale, stream=stream)
+            if self.cache == "fp8":
+                rcb.step_masked_attention_fp8(self.layout, q, k, v, *caches[l], o=o, splits=splits, workspace=ws,
+                                              scale=self.scale, stream=stream)
+            else:
+                rcb.step_masked_attention(self.layout, q, k, v, caches[l][0], caches[l][1], o=o, splits=splits,
+                                          workspace=ws, scale=self.scale, stream=stream)
 
         return self._run(h_live, rcb.ROWS_LIVE, attend, collect, stream=stream)
 

@@ -24,6 +24,7 @@ import torch
 
 import paper_2608_21229_amd as rc
 from oracle import chain as oc
+from oracle import fp8 as of
 from oracle import masks as om
 from synthgen import ANCHOR, REF, TEXT, TARGET, Workload, bf16_normal, draw_chain_weights, draw_hidden, workload
 from tests.parity_util import f64
@@ -216,6 +217,38 @@ def test_chain_matches_oracle(case):
         for l in range(layers):
             check_chain(hs[l], want[l], f"{case} step {step} layer {l} live hidden", l)
             check_chain(hs_full[l], want_full[l], f"{case} full step {step} layer {l} hidden", l)
+
+
+@pytest.mark.parametrize("case", ["tiny", "ragged"])
+def test_chain_fp8_cache_matches_oracle(case):
+    """The chain over the FP8 reference cache: each layer's live rows against
+    the fp64 chain whose step reads the oracle's own quantised-then-dequantised
+    caches (Sec. 3.1, Eq. 2: a layer's cached K/V are its static rows'
+    projections).  The GPU quantises its bf16 K/V, which can differ from the
+    oracle's by one bf16 ulp, so a code may sit one e4m3 step away: the bound
+    is the chain's."""
+    wl, layers, preset = CHAIN_CASES[case]
+    w_qkv, w_o = draw_chain_weights(wl.H, wl.D, layers, wl.seed)
+    layout = rc.Layout(list(wl.segments), preset)
+    ch = rc.Chain(layout, [w.to(DEV) for w in w_qkv], [w.to(DEV) for w in w_o], wl.H, wl.D, cache="fp8")
+    Wq, Wo = [f64(w) for w in w_qkv], [f64(w) for w in w_o]
+    vis = om.PRESETS[preset](wl.kinds)
+    kinds, lens, H, D, scale = wl.kinds, wl.lens, wl.H, wl.D, wl.scale
+    print(f"[case] chain fp8 {case}: B={wl.B} H={H} D={D} segments={wl.segments} layers={layers}", flush=True)
+    h_s, h_l = draw_hidden(wl, 0)
+    caches = ch.prefill(h_s.to(DEV))
+    hs = []
+    ch.step(h_l.to(DEV), caches, collect=hs)
+    torch.cuda.synchronize()
+    _, want_caches = oc.chain_prefill(kinds, lens, vis, f64(h_s), Wq, Wo, H, D, scale)
+    deq = []
+    for kc, vc in want_caches:
+        kq, ks = of.quantize_cache(kc)
+        vq, vs = of.quantize_cache(vc)
+        deq.append((of.dequantize(kq, ks), of.dequantize(vq, vs)))
+    want = oc.chain_step(kinds, lens, vis, f64(h_l), deq, Wq, Wo, H, D, scale)
+    for l in range(layers):
+        check_chain(hs[l], want[l], f"{case} fp8 step layer {l} live hidden", l)
 
 
 ALIGNED = {
