@@ -21,10 +21,14 @@
  *   rc_full_attention         the recompute baseline: all rows over the whole
  *                             sequence under any mask (dense over [LT,X,R] is
  *                             the paper's full-attention Base).
+ * The prefill and step also exist over a cache stored as e4m3 codes
+ * (rc_ref_kv_prefill_fp8, rc_step_masked_attention_fp8), and rc_linear is the
+ * dense projection of the chained synthetic layer built around them.
  *
  * Common conventions
- *   Element type   bf16 for Q, K, V, O and the cache (passed as raw bits);
- *                  fp32 for LSE and workspace.  Arithmetic: bf16 products,
+ *   Element type   bf16 for Q, K, V, O and the cache (passed as raw bits;
+ *                  the FP8 entries store the cache as e4m3 codes with fp32
+ *                  scales); fp32 for LSE and workspace.  Arithmetic: bf16 products,
  *                  fp32 accumulation and softmax, O rounded to bf16 (RNE).
  *   Token layout   Q/K/V are [B, N, H, D] with D contiguous and head stride D;
  *                  `tok_stride` (elements, >= H*D, multiple of 8, <= 2^24) separates
@@ -40,7 +44,8 @@
  *                  only during the call.
  *   Asynchrony     calls enqueue kernels on `stream` and return without
  *                  synchronising.  Results are deterministic: fixed
- *                  reduction order, no atomics.
+ *                  reduction order; the only atomic (the FP8 cache's
+ *                  per-head maximum) is order-independent.
  *   Errors         every function validates all arguments before any HIP
  *                  call and returns an rc_status; on error nothing is
  *                  launched and rc_last_error() (thread-local) describes it.
