@@ -43,6 +43,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -367,23 +368,20 @@ __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t*
 
 // ---------------------------------------------------------------- FP8 cache tiles
 // A cached key tile of the FP8 cache (64 key rows of D e4m3fn codes each for
-// K8 and V8) is loaded into an 8-bit staging stage, widened into the bf16
-// ring stage by the whole work-group (at D = 128 each lane one 16-byte granule
-// of K8 and one of V8), and computed from there exactly like a fresh tile.
-// Widening multiplies by the power-of-two scale, which is exact, so a cached
-// tile contributes attention over the dequantised cache.  Per tile a lane
-// spends 16 conversions (widening every fragment at its use would take 128).
+// K8 and V8) is loaded two tiles ahead of its compute.  K8 stays 8-bit in
+// LDS: S^T = K Q^T runs on the 8-bit MFMA (v_mfma_scale_f32_32x32x64_f8f6f4)
+// against the query rows split into two e4m3 parts (below).  V8 is widened to
+// bf16 one tile ahead by the whole work-group (at D = 128 each lane one
+// 16-byte granule: 8 conversions) into the bf16 ring stage, so P V is the bf16
+// path's.  The scales are powers of two, so widening is exact and the K scale
+// folds into the softmax constant: a cached tile contributes attention over
+// the dequantised cache.
 constexpr int kTile8Bytes = kBN * 128;  // bytes per K8 or V8 staging tile (D <= 128)
-__shared__ __attribute__((aligned(1024))) char g_k8_0[kTile8Bytes];
+// K8: three stages (tile j's codes are read by its QK^T while tile j + 2 loads)
+__shared__ __attribute__((aligned(1024))) char g_k8r[3][kTile8Bytes];
 __shared__ __attribute__((aligned(1024))) char g_v8_0[kTile8Bytes];
-__shared__ __attribute__((aligned(1024))) char g_k8_1[kTile8Bytes];
 __shared__ __attribute__((aligned(1024))) char g_v8_1[kTile8Bytes];
 
-template <int S>
-__device__ __forceinline__ char* k8buf() {
-  if constexpr (S == 0) return g_k8_0;
-  else return g_k8_1;
-}
 template <int S>
 __device__ __forceinline__ char* v8buf() {
   if constexpr (S == 0) return g_v8_0;
@@ -394,20 +392,30 @@ __device__ __forceinline__ uint32_t lds_addr8(const char* ptr) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void*)ptr));
 }
 
-// DMA of one FP8 tile into staging stage S: wave w < D/16 loads the 1 KB chunk
-// w of K8 and of V8, lane l the 16-byte granule p = 64 w + l (row p / (D/16),
-// granule p % (D/16), stored unswizzled at byte 16 p; the cache rows are D
-// bytes apart, so the source offset is 16 p as well).  Rows past the range
-// end lie beyond the record count and arrive as zeros.
-template <int S, int D>
-__device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, uint32_t voff8) {
-  constexpr int kChunks = kBN * (D / 16) / 64;
+// K8 rows in LDS: 16-byte granule g of row r at slot g ^ ((r / (256/D)) &
+// (D/16 - 1)), so the two-granule fragment reads of 32 consecutive rows at
+// one granule pair spread over all bank groups.
+template <int D>
+__device__ __forceinline__ int swz8(int row, int g) {
+  return g ^ ((row / (256 / D)) & (D / 16 - 1));
+}
+
+// DMA of one FP8 tile: wave w < D/16 loads the 1 KB chunk w of K8 (into the
+// K8 stage `ks8`, swizzled) and of V8 (into V8 stage SV at byte 16 p,
+// unswizzled), lane l the 16-byte granule p = 64 w + l (row p / (D/16),
+// granule p % (D/16); cache rows are D bytes apart).  Rows past the range end
+// lie beyond the record count and arrive as zeros.
+template <int SV, int D>
+__device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, int lane, char* ks8) {
+  constexpr int GR8 = D / 16;
+  constexpr int kChunks = kBN * GR8 / 64;
   if (wave >= kChunks) return;
   const int nrec = min(kBN, c.rem) * D;
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
-  dma16(lds_addr8(k8buf<S>() + wave * 1024), voff8, rk);
-  dma16(lds_addr8(v8buf<S>() + wave * 1024), voff8, rv);
+  const int pos = wave * 64 + lane, row = pos / GR8, slot = pos % GR8;
+  dma16(lds_addr8(ks8 + wave * 1024), uint32_t(row * D + swz8<D>(row, slot) * 16), rk);
+  dma16(lds_addr8(v8buf<SV>() + wave * 1024), uint32_t(pos * 16), rv);
 }
 
 // 16 codes (one 8-bit granule: d = 16 g .. 16 g + 15 of key row `row`) times
@@ -415,7 +423,6 @@ __device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, uint32_t 
 template <int D>
 __device__ __forceinline__ void widen_granule(const char* src8, uint16_t* dst, int p, float s) {
   constexpr int GR8 = D / 16, GR = D / 8;
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const u32x4 w = *reinterpret_cast<const u32x4*>(src8 + p * 16);
   uint32_t e[8];
 #pragma unroll
@@ -428,19 +435,109 @@ __device__ __forceinline__ void widen_granule(const char* src8, uint16_t* dst, i
   *reinterpret_cast<u32x4*>(dst + row * D + swz(row, 2 * g + 1, GR) * 8) = u32x4{e[4], e[5], e[6], e[7]};
 }
 
-// Widen staging stage S into bf16 ring stage S.  The K8 and V8 tiles hold
-// 64 D / 16 granules each: at D = 128 thread i takes granule i of both, at
-// D = 64 the first half of the threads K8 and the second half V8.
+// Widen V8 stage S into bf16 V stage S: thread i takes granule i (64 D / 16
+// granules: every thread at D = 128, the first half at D = 64).
 template <int S, int D>
-__device__ __forceinline__ void widen_tile8(int tid, float sk, float sv) {
+__device__ __forceinline__ void widen_v8(int tid, float sv) {
   constexpr int NG = kBN * (D / 16);
-  if constexpr (NG == kThreads) {
-    widen_granule<D>(k8buf<S>(), kbuf<S>(), tid, sk);
-    widen_granule<D>(v8buf<S>(), vbuf<S>(), tid, sv);
-  } else {
-    static_assert(2 * NG == kThreads, "one granule per thread");
-    if (tid < NG) widen_granule<D>(k8buf<S>(), kbuf<S>(), tid, sk);
-    else widen_granule<D>(v8buf<S>(), vbuf<S>(), tid - NG, sv);
+  static_assert(NG <= kThreads, "one granule per thread");
+  if (NG == kThreads || tid < NG) widen_granule<D>(v8buf<S>(), vbuf<S>(), tid, sv);
+}
+
+// This lane's query row in e4m3 for the 8-bit QK^T: chunk c holds
+// d = 64 c + 32 hh .. +31 (hh = lane / 32; the K8 fragment of the same lane
+// holds the same d).  The row is scaled by 2^-e, e the smallest integer with
+// amax 2^-e <= 448, and split as hi + lo / 16 with both parts e4m3 (round to
+// nearest even): a bf16 value has 8 significant bits, hi keeps 4 and the
+// remainder has at most 4, so the split is exact except for elements below
+// about 2^-11 of the row's largest, whose lowest bits may go (an error below
+// 2^-20 of the row's largest).
+template <int D>
+struct Q8 {
+  i32x8 hi[D / 64], lo[D / 64];
+};
+
+__device__ __forceinline__ int e4m3_exponent(float amax) {
+  if (!(amax > 0.f)) return 0;
+  int k;
+  const float m = frexpf(amax, &k);  // amax = m 2^k, 0.5 <= m < 1; 448 = 0.875 * 2^9
+  return m <= 0.875f ? k - 9 : k - 8;
+}
+
+template <int D>
+__device__ __forceinline__ int make_q8(const uint16_t* qrow, bool row_ok, int hh, Q8<D>& q8) {
+  constexpr int NC = D / 64;
+  float x[NC][32];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const u32x4 raw = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * c + 32 * hh + 8 * g)
+                               : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        x[c][8 * g + 2 * w] = __uint_as_float(raw[w] << 16);
+        x[c][8 * g + 2 * w + 1] = __uint_as_float(raw[w] & 0xffff0000u);
+      }
+    }
+  float amax = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = fmaxf(amax, fabsf(x[c][i]));
+  amax = max_halves(amax);
+  const int e = e4m3_exponent(amax);
+  const float sc = ldexpf(1.f, -e);
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const float t0 = x[c][4 * w] * sc, t1 = x[c][4 * w + 1] * sc;
+      const float t2 = x[c][4 * w + 2] * sc, t3 = x[c][4 * w + 3] * sc;
+      int hi = __builtin_amdgcn_cvt_pk_fp8_f32(t0, t1, 0, false);
+      hi = __builtin_amdgcn_cvt_pk_fp8_f32(t2, t3, hi, true);
+      const auto b01 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false);
+      const auto b23 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
+      int lo = __builtin_amdgcn_cvt_pk_fp8_f32((t0 - b01[0]) * 16.f, (t1 - b01[1]) * 16.f, 0, false);
+      lo = __builtin_amdgcn_cvt_pk_fp8_f32((t2 - b23[0]) * 16.f, (t3 - b23[1]) * 16.f, lo, true);
+      q8.hi[c][w] = hi;
+      q8.lo[c][w] = lo;
+    }
+  return e;
+}
+
+// K8 fragment of key block kb, chunk c: row kb*32 + lane%32, bytes
+// d = 64 c + 32 hh .. +31 (two swizzled granules).
+template <int D>
+__device__ __forceinline__ i32x8 k8_frag(const char* ks8, int lane, int kb, int c) {
+  const int row = kb * 32 + (lane & 31);
+  const int g = 4 * c + 2 * (lane >> 5);
+  const u32x4 a = *reinterpret_cast<const u32x4*>(ks8 + row * D + swz8<D>(row, g) * 16);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(ks8 + row * D + swz8<D>(row, g + 1) * 16);
+  return i32x8{int(a[0]), int(a[1]), int(a[2]), int(a[3]), int(b[0]), int(b[1]), int(b[2]), int(b[3])};
+}
+
+// S^T (in units of s_K 2^e) of one FP8 tile: per 32-key block and 64-wide
+// chunk of d, one 8-bit MFMA against hi (scale 1) and one against lo (scale
+// 2^-4), accumulating into the same registers.
+template <int D>
+__device__ __forceinline__ void s_part8(const char* ks8, int lane, const Q8<D>& q8, f32x16 (&sacc)[2]) {
+  constexpr int NC = D / 64;
+  constexpr int NF = 2 * NC;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+  i32x8 a[2];
+  a[0] = k8_frag<D>(ks8, lane, 0, 0);
+  sched_fence();
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int kb = f / NC, c = f % NC;
+    if (f + 1 < NF) a[(f + 1) & 1] = k8_frag<D>(ks8, lane, (f + 1) / NC, (f + 1) % NC);
+    sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.hi[c], sacc[kb], 0, 0, 0, 127, 0, 127);
+    sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.lo[c], sacc[kb], 0, 0, 0, 127, 0, 123);
+    sched_fence();
   }
 }
 
@@ -521,44 +618,51 @@ __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b,
 }
 
 // Step j of n of the FP8 ring: wait for tile j + 1's loads, barrier (tile
-// j's widened values are visible; bf16 stage (j + 1) % 2 and staging stage
-// j % 2 are free), load tile j + 2 into staging stage j % 2, compute tile j
-// from bf16 stage j % 2, then widen tile j + 1 into bf16 stage (j + 1) % 2
-// (after the compute: the tile's MFMAs start right after the barrier; 2.5%
-// faster than widening first, measured).
+// j's widened V is visible; bf16 V stage (j + 1) % 2, V8 stage j % 2 and K8
+// stage (j + 2) % 3 are free), load tile j + 2, compute tile j, then widen
+// tile j + 1's V into bf16 stage (j + 1) % 2 (after the compute, so that the
+// tile's MFMAs start right after the barrier).
 template <int S, int D>
 __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int tid, int wave, int lane,
-                                           bool wave_active, uint32_t voff8, Cursor& icur, Cursor& ccur, float sk,
-                                           float sv, const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
-                                           float& m_used, float& lsum, float c) {
+                                           bool wave_active, Cursor& icur, Cursor& ccur, float sv, const Q8<D>& q8,
+                                           f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float cq) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   ring_barrier();
   if (j + 2 < n) {
-    issue_tile8<S, D>(icur, wave, voff8);
+    issue_tile8<S, D>(icur, wave, lane, g_k8r[(j + 2) % 3]);
     if (j + 3 < n) cursor_next(p, icur);
   }
   const int valid = tile_valid(ccur);
-  if (wave_active) tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
-  if (j + 1 < n) widen_tile8<S ^ 1, D>(tid, sk, sv);
+  if (wave_active) {
+    f32x16 sacc[2];
+    bf16x8 pf[4];
+    s_part8<D>(g_k8r[j % 3], lane, q8, sacc);
+    softmax_part<D>(lane, valid, sacc, pf, oacc, m_used, lsum, cq);
+    pv_part<D>(vbuf<S>(), lane, pf, oacc);
+  }
+  if (j + 1 < n) widen_v8<S ^ 1, D>(tid, sv);
   if (j + 1 < n) cursor_next(p, ccur);
 }
 
 // The ring over FP8 cache tiles [kt_begin, kt_end): loads run two tiles
-// ahead of the compute, widening one tile ahead.
+// ahead of the compute, V widening one tile ahead.  qrow: this lane's query
+// row (bf16), read again here to build its e4m3 parts.
 template <int D>
 __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
-                                          int tid, int wave, int lane, bool wave_active, float sk, float sv,
-                                          const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
+                                          int tid, int wave, int lane, bool wave_active, const uint16_t* qrow,
+                                          bool row_ok, float sk, float sv, f32x16 (&oacc)[D / 32], float& m_used,
                                           float& lsum, float c) {
   const int n = kt_end - kt_begin;
   if (n <= 0) return;
-  const uint32_t voff8 = uint32_t(wave * 64 + lane) * 16u;
+  Q8<D> q8;
+  const int e = make_q8<D>(qrow, row_ok, lane >> 5, q8);
+  const float cq = c * sk * ldexpf(1.f, e);  // scores are s_K 2^e times the accumulated ones
   Cursor icur = cursor_at(p, qs, kt_begin, b, h);
   Cursor ccur = icur;
-  issue_tile8<0, D>(icur, wave, voff8);
+  issue_tile8<0, D>(icur, wave, lane, g_k8r[0]);
   if (n > 1) {
     cursor_next(p, icur);
-    issue_tile8<1, D>(icur, wave, voff8);
+    issue_tile8<1, D>(icur, wave, lane, g_k8r[1]);
     if (n > 2) cursor_next(p, icur);
     // tile 0 landed, tile 1 (two loads per loading wave) may be in flight
     asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
@@ -566,12 +670,11 @@ __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
   ring_barrier();
-  widen_tile8<0, D>(tid, sk, sv);
+  widen_v8<0, D>(tid, sv);
   for (int j = 0; j < n; j += 2) {
-    ring8_step<0, D>(p, j, n, tid, wave, lane, wave_active, voff8, icur, ccur, sk, sv, qf, oacc, m_used, lsum, c);
+    ring8_step<0, D>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
     if (j + 1 >= n) break;
-    ring8_step<1, D>(p, j + 1, n, tid, wave, lane, wave_active, voff8, icur, ccur, sk, sv, qf, oacc, m_used, lsum,
-                     c);
+    ring8_step<1, D>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
   }
 }
 
@@ -656,8 +759,9 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
     const int mid = min(max(kt_split, kt_begin), kt_end);
     run_ring<D>(p, qs, b, h, kt_begin, mid, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c);
     if (kt_begin < mid && mid < kt_end) ring_barrier();  // the first ring's stages are read no more
-    run_ring8<D>(p, qs, b, h, mid, kt_end, wave * 64 + lane, wave, lane, wave_active, sk, sv, qf, oacc, m_used, lsum,
-                 c);
+    const uint16_t* qrow = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row) * p.q_st + int64_t(h) * D;
+    run_ring8<D>(p, qs, b, h, mid, kt_end, wave * 64 + lane, wave, lane, wave_active, qrow, row_ok, sk, sv, oacc,
+                 m_used, lsum, c);
   } else {
     run_ring<D>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c);
   }
