@@ -30,6 +30,11 @@
 // tile cursor keeps the current key range's pointers in scalar registers, so
 // issuing a tile needs no reads of the range table; the K and V fragment
 // reads are software-pipelined kPrefetch MFMAs ahead of their use.
+//
+// Over the FP8 cache (the kF8 instantiation) the fresh key ranges run through
+// that ring and the cached ranges through a second one: K8 stays 8-bit and
+// S^T = K Q^T runs on the 8-bit MFMA against a two-part e4m3 split of Q, and
+// V8 is widened to bf16 once per tile (see the FP8 cache tiles section).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
