@@ -108,6 +108,14 @@ def test_fp8_headline():
     check_fp8_request(workload("ref5"), "perref", every=97)
 
 
+def test_fp8_cfg_two_branch_batch():
+    """Both guidance branches in one batch at the headline shape: the step's
+    entries run as consecutive launches, each with its own scales."""
+    wl = workload("ref5")
+    wl = Workload("ref5_cfg_fp8", 2, wl.H, wl.D, wl.segments, seed=7)
+    check_fp8_request(wl, "perref", every=113, splits=1)
+
+
 def test_fp8_three_head_share_split_kv():
     wl = workload("ref5")
     wl = Workload("ref5_h3_fp8", 1, 3, 128, wl.segments, seed=19)

@@ -157,6 +157,37 @@ def test_ref5_cfg_two_branch_batch():
     check_request(wl, "perref", every=113)
 
 
+def test_batch_entries_equal_single_calls():
+    """Two guidance branches at the headline shape: each batch entry of the
+    B = 2 prefill, step (its grids fill the chip per entry, so the entries run
+    as consecutive launches) and full recompute, with LSE, equals the B = 1
+    call on that entry's slice bit for bit."""
+    from synthgen import Workload
+    wl = workload("ref5")
+    wl = Workload("ref5_cfg", 2, wl.H, wl.D, wl.segments, std=wl.std, seed=7)
+    inp = draw_inputs(wl)
+    L = layout_for(inp, "perref")
+    qs, ks, vs = (t.to(DEV) for t in inp.static)
+    ql, kl, vl = (t.to(DEV) for t in inp.live)
+    qa, ka, va = (full_sequence(inp, i).to(DEV) for i in range(3))
+    o2, l2, kc2, vc2 = rc.ref_kv_prefill(L, qs, ks, vs, scale=wl.scale, want_lse=True)
+    s2, sl2 = rc.step_masked_attention(L, ql, kl, vl, kc2, vc2, scale=wl.scale, splits=1, want_lse=True)
+    f2, fl2 = rc.full_attention(L, qa, ka, va, scale=wl.scale, want_lse=True)
+    for b in range(2):
+        sl = slice(b, b + 1)
+        o1, l1, kc1, vc1 = rc.ref_kv_prefill(L, qs[sl].contiguous(), ks[sl].contiguous(), vs[sl].contiguous(),
+                                             scale=wl.scale, want_lse=True)
+        s1, sl1 = rc.step_masked_attention(L, ql[sl].contiguous(), kl[sl].contiguous(), vl[sl].contiguous(),
+                                           kc1, vc1, scale=wl.scale, splits=1, want_lse=True)
+        f1, fl1 = rc.full_attention(L, qa[sl].contiguous(), ka[sl].contiguous(), va[sl].contiguous(),
+                                    scale=wl.scale, want_lse=True)
+        torch.cuda.synchronize()
+        for name, x2, x1 in (("prefill O", o2, o1), ("prefill LSE", l2, l1), ("K cache", kc2, kc1),
+                             ("V cache", vc2, vc1), ("step O", s2, s1), ("step LSE", sl2, sl1),
+                             ("full O", f2, f1), ("full LSE", fl2, fl1)):
+            assert torch.equal(x2[sl], x1), f"batch entry {b}: {name} differs from the single call"
+
+
 def test_ref5_full_recompute_and_step_rows():
     """Full recompute (dense Base over [LT, X, R], and the same cacheable mask)
     on sampled rows; the step's rows equal the same-mask full recompute's
