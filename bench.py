@@ -48,22 +48,31 @@ def source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(config: str):
-    """HBM bytes per step launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source; otherwise None."""
+def measured_counters(config: str):
+    """(HBM bytes per step launch, MFMA-busy fraction of the kernel's cycles)
+    from the committed rocprofv3 counter summary, if it was taken on the
+    current kernel source; otherwise (None, None)."""
     if config != "ref5" or not os.path.exists(TRAFFIC_FILE):
-        return None
+        return None, None
     vals = {}
     for line in open(TRAFFIC_FILE):
         if ":" in line and not line.lstrip().startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     if vals.get("kernel_source_sha256_16") != source_hash():
-        return None
-    try:
-        return float(vals["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+        return None, None
+    out = []
+    for key in ("hbm_bytes_per_launch", "mfma_busy_fraction"):
+        try:
+            out.append(float(vals[key]))
+        except (KeyError, ValueError):
+            out.append(None)
+    return tuple(out)
+
+
+def measured_traffic(config: str):
+    """HBM bytes per step launch (see measured_counters)."""
+    return measured_counters(config)[0]
 
 
 def gen_bf16(torch, shape, gen, std, device):
@@ -487,7 +496,8 @@ def main():
         side = extras(torch, rc, wl, gen, dev, static[0], live[0][0], step_avg)
 
     # the committed counter summary covers the bf16-cache step kernel
-    traffic = measured_traffic(args.config) if splits == 1 and not args.fp8_cache else None
+    traffic, mfma_busy = (measured_counters(args.config) if splits == 1 and not args.fp8_cache
+                          else (None, None))
     f8 = "true" if args.fp8_cache else "false"
     cached_bytes = 1 if args.fp8_cache else 2
     out = {
@@ -529,6 +539,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": traffic,
+            "mfma_busy_fraction_rocprof": mfma_busy,
             "algorithmic_bytes_per_launch": 2.0 * B * H * D * (4 * n_live + cached_bytes * n_cached),
             "useful_flop_per_launch": flop_step,
         },
