@@ -89,7 +89,7 @@ rc_status hip_status(int err, const char* what) {
 }
 
 size_t balanced_workspace_bytes(int32_t D) {
-  return size_t(2) * kBalancedWGs * kBM * size_t(D + 2) * sizeof(float);
+  return size_t(2) * kBalancedWGs * rows_per_wg(kQBBalanced) * size_t(D + 2) * sizeof(float);
 }
 
 // A bf16 key source from element strides (batch, head, token) shared by K and V.
@@ -131,14 +131,18 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   RC_TRY(check_ptr(v_static, "v_static"));
   RC_TRY(check_ptr(o_static, "o_static"));
   RC_TRY(check_lse(lse_static, "lse_static"));
-  if (n_cached > 0) {
-    RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
-    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8" : "v_cache"));
-    if (fp8) RC_TRY(check_lse(kv_scale, "kv_scale"));
-    if (fp8 && !kv_scale) {
+  if (fp8) {
+    // the scales are required whatever the cache size, so that a caller's
+    // missing buffer is caught here rather than on the device
+    if (!kv_scale) {
       set_error("kv_scale is null");
       return RC_ERR_ARG;
     }
+    RC_TRY(check_lse(kv_scale, "kv_scale"));
+  }
+  if (n_cached > 0) {
+    RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
+    RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8" : "v_cache"));
     if (fp8 && n_cached > kFp8MaxKeys) {
       set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_cached,
                 (long long)kFp8MaxKeys);
@@ -148,6 +152,7 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
+  p.bm = rows_per_wg(kQBPlain);
   RC_TRY(plan(L, RC_ENTRY_PREFILL, p));
   RC_TRY(check_grid(p));
   p.q = static_cast<const uint16_t*>(q_static);
@@ -242,6 +247,14 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
     set_error("the balanced schedule is not available with the FP8 cache");
     return RC_ERR_UNSUPPORTED;
   }
+  if (fp8) {
+    // required whatever the cache size (see the prefill)
+    if (!kv_scale) {
+      set_error("kv_scale is null");
+      return RC_ERR_ARG;
+    }
+    RC_TRY(check_lse(kv_scale, "kv_scale"));
+  }
   if (n_live == 0) return RC_OK;  // no LT/X segment: nothing to attend
   RC_TRY(check_ptr(q_live, "q_live"));
   RC_TRY(check_ptr(k_live, "k_live"));
@@ -252,11 +265,6 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
     RC_TRY(check_ptr(k_cache, fp8 ? "k_cache8" : "k_cache"));
     RC_TRY(check_ptr(v_cache, fp8 ? "v_cache8" : "v_cache"));
     if (fp8) {
-      if (!kv_scale) {
-        set_error("kv_scale is null");
-        return RC_ERR_ARG;
-      }
-      RC_TRY(check_lse(kv_scale, "kv_scale"));
       if (n_cached > kFp8MaxKeys) {
         set_error("FP8 cache of %lld keys per (batch, head) exceeds %lld", (long long)n_cached,
                   (long long)kFp8MaxKeys);
@@ -264,14 +272,16 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
       }
     }
   }
+  // the automatic choice is the one rc_step_auto_splits reports (for either
+  // cache format)
+  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
+  const bool balanced = splits == kSplitsBalanced;
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
+  p.bm = rows_per_wg(fp8 ? kQBFp8 : balanced ? kQBBalanced : kQBPlain);
   RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
-  // the automatic choice is the one rc_step_auto_splits reports
-  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
   p.splits = splits;
-  const bool balanced = p.splits == kSplitsBalanced;
   if (balanced) {
     p.units = int64_t(B) * H * p.units_bh;
     p.bal_wgs = kBalancedWGs;
@@ -302,7 +312,7 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
       return RC_ERR_WORKSPACE;
     }
     p.ws_o = static_cast<float*>(workspace);
-    p.ws_ml = p.ws_o + size_t(2) * kBalancedWGs * kBM * D;
+    p.ws_ml = p.ws_o + size_t(2) * kBalancedWGs * rows_per_wg(kQBBalanced) * D;
     RC_TRY(check_blocks((int64_t(B) * H * n_live * (D / 4) + 255) / 256, "balanced merge"));
     RC_TRY(hip_status(launch_attention_balanced(p, D, stream), "step attention launch"));
     RC_TRY(hip_status(launch_combine_balanced(p, D, stream), "balanced merge launch"));
@@ -368,6 +378,7 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
   memset(&p, 0, sizeof p);
   p.B = B;
   p.H = H;
+  p.bm = rows_per_wg(kQBPlain);
   if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
   return auto_splits(p);
 }
@@ -415,6 +426,7 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
+  p.bm = rows_per_wg(kQBPlain);
   RC_TRY(plan(L, RC_ENTRY_FULL, p));
   RC_TRY(check_grid(p));
   p.q = static_cast<const uint16_t*>(q);

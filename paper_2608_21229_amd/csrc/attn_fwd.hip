@@ -6,33 +6,38 @@
 // hands every work-group a BM-row query tile inside one segment and the list
 // of visible key ranges; invisible segments are never loaded.
 //
-// Work-group = kWaves waves of 64 lanes (8 by default: BM = 256 rows, one
-// work-group and two waves per SIMD on each CU); each wave owns 32 query rows.
+// Work-group = 8 waves of 64 lanes, one work-group and two waves per SIMD on
+// each CU.  A wave owns QB blocks of 32 query rows (two in the bf16 kernels:
+// BM = 512; one in the FP8-cache step and the balanced schedule: BM = 256).
 // Per 64-key tile:
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = the
-//                   wave's Q rows held in registers for the whole kernel.
-//                   The 32x32 accumulator puts one query per lane (lane % 32)
-//                   and 16 keys per lane, so the row max needs only in-lane
-//                   max plus one exchange between the two 32-lane halves.
+//                   wave's Q rows held in registers for the whole kernel; each
+//                   K fragment feeds one MFMA per query block.  The 32x32
+//                   accumulator puts one query per lane (lane % 32) and 16
+//                   keys per lane, so row reductions stay in the lane plus
+//                   one exchange between the two 32-lane halves.
 //   online softmax  exp2 with scale*log2(e) folded into one FMA; the running
-//                   max is refreshed lazily (only when a row's max grows by
-//                   more than 2^8), which is exact because the same stale max
-//                   scales both the sum and the accumulator.
+//                   max is refreshed lazily (only when a row's weights would
+//                   grow past a bound), which is exact because the same stale
+//                   max scales both the sum and the accumulator.
 //   O^T += V^T P^T  A = V^T read from row-major V in LDS with the gfx950
 //                   transpose read ds_read_b64_tr_b16, B = P^T straight from
 //                   the S^T accumulator registers (bf16), so the output also
 //                   has one query per lane and the softmax statistics never
 //                   leave their lane.
-// K/V tiles stream through a ring of kStages LDS stages (2 by default) with
-// direct global->LDS buffer loads (16 bytes per lane, 16 lanes per 256-byte
-// row), placed with an XOR swizzle at 16-byte granularity that keeps both the
-// 128-bit K reads and the transpose V reads free of bank conflicts.  The
-// tile cursor keeps the current key range's pointers in scalar registers, so
-// issuing a tile needs no reads of the range table; the K and V fragment
-// reads are software-pipelined kPrefetch MFMAs ahead of their use.
+// K/V tiles arrive by direct global->LDS buffer loads (16 bytes per lane, 16
+// lanes per 256-byte row), placed with an XOR swizzle at 16-byte granularity
+// that keeps both the 128-bit K reads and the transpose V reads free of bank
+// conflicts.  The tile cursor keeps the current key range's pointers in
+// scalar registers, so issuing a tile needs no reads of the range table.
+//
+// With two query blocks per wave a tile is computed as two 32-key sub-tiles,
+// and the two waves of each SIMD run half a phase apart (the ping-pong ring):
+// one issues MFMAs while the other does its softmax.  With one block per wave
+// every wave loads and computes whole tiles behind one barrier per tile.
 //
 // Over the FP8 cache (the kF8 instantiation) the fresh key ranges run through
-// that ring and the cached ranges through a second one: K8 stays 8-bit and
+// the bf16 ring and the cached ranges through a second one: K8 stays 8-bit and
 // S^T = K Q^T runs on the 8-bit MFMA against a two-part e4m3 split of Q, and
 // V8 is widened to bf16 once per tile (see the FP8 cache tiles section).
 #include <hip/hip_runtime.h>
@@ -48,6 +53,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -154,8 +160,8 @@ __shared__ __attribute__((aligned(1024))) uint16_t g_k0[kTileElems];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v0[kTileElems];
 __shared__ __attribute__((aligned(1024))) uint16_t g_k1[kTileElems];
 __shared__ __attribute__((aligned(1024))) uint16_t g_v1[kTileElems];
-__shared__ __attribute__((aligned(1024))) uint16_t g_k2[kStages > 2 ? kTileElems : 8];
-__shared__ __attribute__((aligned(1024))) uint16_t g_v2[kStages > 2 ? kTileElems : 8];
+__shared__ __attribute__((aligned(1024))) uint16_t g_k2[kTileElems];  // third stage: ping-pong ring only
+__shared__ __attribute__((aligned(1024))) uint16_t g_v2[kTileElems];
 
 template <int S>
 __device__ __forceinline__ uint16_t* kbuf() {
@@ -207,10 +213,13 @@ template <int D>
 __device__ __forceinline__ void issue_tile(const Cursor& c, int wave, const uint32_t* voff0, const uint32_t* voff1,
                                            uint16_t* ks, uint16_t* vs) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
-  const int valid = min(kBN, c.rem);
-  const int nrec = valid * c.st;
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
+  // record count: at most 64 tokens of at most 2^25 bytes (the stride limit
+  // the API enforces), i.e. at most 2^31, which fits the unsigned 32-bit field
+  const uint32_t nrec = uint32_t(min(kBN, c.rem)) * uint32_t(c.st);
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
   // the lane offsets are passed straight from the long-lived per-source
   // registers (a uniform branch, not a select into a temporary)
   if (c.src == 0) {
@@ -232,60 +241,118 @@ __device__ __forceinline__ void issue_tile(const Cursor& c, int wave, const uint
 
 __device__ __forceinline__ int tile_valid(const Cursor& c) { return min(kBN, c.rem); }
 
-constexpr int kPrefetch = 3;  // LDS fragment reads kept in flight ahead of the MFMA that uses them
+// ---------------------------------------------------------------- tile compute
+// A wave owns QB blocks of 32 query rows.  Every K or V^T fragment it reads
+// from LDS feeds one MFMA per block, so two blocks halve the LDS bytes per
+// MFMA.  With two blocks the score accumulators of both must fit next to the
+// output accumulators within the register budget of two waves per SIMD, so a
+// 64-key tile is computed as two 32-key sub-tiles (QK^T, softmax, PV each).
+template <int QB>
+struct Blk {
+  static constexpr int kSub = QB == 1 ? kBN : 32;  // keys per sub-tile
+  static constexpr int kKB = kSub / 32;            // 32-key blocks per sub-tile
+  static constexpr int kPF = QB == 1 ? 3 : 2;      // fragment reads in flight ahead of their MFMAs
+  static constexpr int kRows = 32 * QB * kWaves;   // query rows per work-group
+};
 
 // Scheduling fence: the compiler moves no instruction across it, so the
-// software-pipelined order below (reads issued kPrefetch MFMAs ahead) stays.
+// software-pipelined order below (reads issued kPF fragments ahead) stays.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
-// K fragment f = kb * NDC + dc of S^T = K Q^T: rows kb*32 + lane%32,
-// granule 2 dc + lane/32.
+// Per-lane LDS byte offsets of the fragment reads inside a tile.  The swizzle
+// XORs granule bits with row bits, so a fragment's address is the lane's base
+// XOR a compile-time constant (the XOR touches only in-row bits), plus a
+// constant row offset that the LDS instruction's offset field absorbs.
+struct FragBase {
+  uint32_t k;       // K fragment: row lane%32, granule lane/32
+  uint32_t v0, v1;  // V^T fragment: the two transpose reads (rows r0 and r0 + 8)
+};
+
 template <int D>
-__device__ __forceinline__ bf16x8 k_frag(const uint16_t* ks, int lane, int f) {
+__device__ __forceinline__ FragBase frag_base(int lane) {
   constexpr int GR = D / 8;
-  constexpr int NDC = D / 16;
-  const int kb = f / NDC, dc = f % NDC;
-  const int krow = kb * 32 + (lane & 31);
-  return *reinterpret_cast<const bf16x8*>(ks + krow * D + swz(krow, 2 * dc + (lane >> 5), GR) * 8);
+  const int hh = lane >> 5, li = lane & 15;
+  FragBase fb;
+  {
+    const int row = lane & 31;
+    const int x = (((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1);
+    fb.k = uint32_t(row * D * 2 + 16 * (x ^ hh));  // granule 2 dc + hh = (2 dc) ^ hh
+  }
+  // V^T: rows r0 = 4 hh + li/4 (+ 8), d = 16 ((lane/16)&1) + 4 (li%4) inside a
+  // 32-wide block: granule c = 2 ((lane/16)&1) + (li%4)/2, element 4 (li%2)
+  const int c = 2 * ((lane >> 4) & 1) + ((li & 3) >> 1);
+  const int r0 = 4 * hh + (li >> 2), r1 = r0 + 8;
+  const int x0 = (((r0 & 3) << 2) | ((r0 >> 2) & 3)) & (GR - 1);
+  const int x1 = (((r1 & 3) << 2) | ((r1 >> 2) & 3)) & (GR - 1);
+  fb.v0 = uint32_t(r0 * D * 2 + 16 * (c ^ x0) + 8 * (li & 1));
+  fb.v1 = uint32_t(r1 * D * 2 + 16 * (c ^ x1) + 8 * (li & 1));
+  return fb;
 }
 
-// S^T = K Q^T for one 64-key tile (two 32x32 accumulators).
+// The fragment bases of one compute phase.  They are hidden from
+// loop-invariant code motion, so each phase recomputes its fragment addresses
+// (one XOR per read) instead of keeping all of them live in registers.
 template <int D>
-__device__ __forceinline__ void s_part(const uint16_t* ks, int lane, const bf16x8 (&qf)[D / 16],
-                                       f32x16 (&sacc)[2]) {
+__device__ __forceinline__ FragBase phase_base(int lane) {
+  FragBase fb = frag_base<D>(lane);
+  asm volatile("" : "+v"(fb.k), "+v"(fb.v0), "+v"(fb.v1));
+  return fb;
+}
+
+// K fragment f = kb * NDC + dc of S^T = K Q^T: rows kb*32 + lane%32 of the
+// tile, granule 2 dc + lane/32.
+template <int D>
+__device__ __forceinline__ bf16x8 k_frag(const uint16_t* ks, const FragBase& fb, int f) {
   constexpr int NDC = D / 16;
-  constexpr int NF = 2 * NDC;
-  constexpr int PF = kPrefetch;
+  const int kb = f / NDC, dc = f % NDC;
+  const char* p = reinterpret_cast<const char*>(ks) + (fb.k ^ uint32_t(32 * dc)) + kb * 32 * D * 2;
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+// S^T = K Q^T for sub-tile j (kKB 32x32 accumulators per query block).
+template <int D, int QB>
+__device__ __forceinline__ void s_part(const uint16_t* ks, const FragBase& fb, int j,
+                                       const bf16x8 (&qf)[QB][D / 16], f32x16 (&sacc)[QB][Blk<QB>::kKB]) {
+  constexpr int KB = Blk<QB>::kKB;
+  constexpr int NDC = D / 16;
+  constexpr int NF = KB * NDC;
+  constexpr int PF = Blk<QB>::kPF;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
   bf16x8 a[PF + 1];
 #pragma unroll
-  for (int f = 0; f < PF && f < NF; ++f) a[f] = k_frag<D>(ks, lane, f);
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = k_frag<D>(ks, fb, j * NF + f);
   sched_fence();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int kb = f / NDC, dc = f % NDC;
-    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], qf[dc], sacc[kb], 0, 0, 0);
-    if (f + PF < NF) a[(f + PF) % (PF + 1)] = k_frag<D>(ks, lane, f + PF);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+      sacc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], qf[qb][dc], sacc[qb][kb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = k_frag<D>(ks, fb, j * NF + f + PF);
     sched_fence();
   }
 }
 
-// Online softmax of one S^T tile (row = this lane's query) into P^T (bf16).
-template <int D>
-__device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)[2], bf16x8 (&pf)[4],
-                                             f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float c) {
-  constexpr int NB = D / 32;
-  const int hh = lane >> 5;
-  // ragged tail: keys past the end of the range score -inf.  Slot r of half
-  // hh holds key kb*32 + 8 (r/4) + 4 hh + r%4: compare the lane-independent
-  // part against valid - 4 hh.
-  if (valid < kBN) {
-    const int lim = valid - 4 * hh;
+// Online softmax of one S^T sub-tile, in three parts per query block (row =
+// this lane's query): the tile's row max, the lazy rescale, and P^T = exp2 in
+// bf16 with the row sum.
+//
+// Row max of one block's sub-tile in log2 units (c: the factor from
+// accumulator units to log2 units).  Keys past the end of the range (valid:
+// keys of the sub-tile inside the range) score -inf first: slot r of half hh
+// holds key kb*32 + 8 (r/4) + 4 hh + r%4, so the lane-independent part is
+// compared against valid - 4 hh.
+template <int KB>
+__device__ __forceinline__ float tile_max(int lane, int valid, f32x16 (&sacc)[KB], float c) {
+  if (valid < 32 * KB) {
+    const int lim = valid - 4 * (lane >> 5);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kb * 32 + 8 * (r >> 2) + (r & 3);
@@ -294,22 +361,33 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
   }
   float mx = sacc[0][0];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-  const float mt = max_halves(mx) * c;
-  if (__any(mt > m_used + kLazyThreshold)) {
-    const float m_new = fmaxf(m_used, mt);
-    const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
-    lsum *= alpha;
+  return max_halves(mx) * c;
+}
+
+// Move the running max to max(m_used, mt): exact, since the same factor
+// scales the row sum and the accumulator.
+template <int D>
+__device__ __forceinline__ void rescale(f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float mt) {
+  const float m_new = fmaxf(m_used, mt);
+  const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
+  lsum *= alpha;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+  for (int nb = 0; nb < D / 32; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
-    m_used = m_new;
-  }
+    for (int r = 0; r < 16; ++r) oacc[nb][r] *= alpha;
+  m_used = m_new;
+}
+
+// p = 2^(s c - m_used) into P^T (bf16, the B operand of the P V MFMAs) and
+// the unrounded sum.
+template <int KB>
+__device__ __forceinline__ void exp_part(const f32x16 (&sacc)[KB], bf16x8 (&pf)[2 * KB], float m_used, float& lsum,
+                                         float c) {
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][r], c, -m_used));
@@ -318,57 +396,156 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
     }
 }
 
+// All query blocks of a sub-tile.  The running max is refreshed lazily, only
+// when some row's tile max exceeds it by more than 2^8; one wave-uniform
+// branch covers all blocks (a block whose max did not grow is rescaled too,
+// by 1 or by the exact factor).  A sub-tile whose keys all lie past the range
+// end (valid <= 0) contributes p = 0 once the running max is finite, which
+// the first sub-tile of a segment's keys (valid >= 1) guarantees.
+template <int D, int QB>
+__device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)[QB][Blk<QB>::kKB],
+                                             bf16x8 (&pf)[QB][2 * Blk<QB>::kKB], f32x16 (&oacc)[QB][D / 32],
+                                             float (&m_used)[QB], float (&lsum)[QB], const float (&c)[QB]) {
+  float mt[QB];
+  bool grow = false;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    mt[qb] = tile_max(lane, valid, sacc[qb], c[qb]);
+    grow = grow || mt[qb] > m_used[qb] + kLazyThreshold;
+  }
+  if (__any(grow)) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) rescale<D>(oacc[qb], m_used[qb], lsum[qb], mt[qb]);
+  }
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) exp_part(sacc[qb], pf[qb], m_used[qb], lsum[qb], c[qb]);
+}
+
+// Optimistic online softmax of one 32-key sub-tile for both query blocks of
+// a wave, used by the ping-pong ring.  While the other wave's MFMAs run, a
+// wave issues a VALU instruction every ~8 cycles and a v_exp_f32 every ~10,
+// so this phase must be short and free of long dependent chains.  The common
+// case does no max reduction: the arguments a = s c - m_used for both blocks
+// (in place), then p = 2^a packed to bf16 P^T, and the row sum over the packed
+// weights (the values the P V product uses) with v_dot2_f32_bf16 in four
+// independent chains.  If some lane's partial sum leaves [0, 2^16] or is not a
+// number, the running max moves up by max(0, max a) and the weights are
+// recomputed from the shifted arguments (exact up to one fp32 rounding of the
+// argument).  So every weight stays below 2^16 and the fp32 accumulators
+// cannot overflow.  The first sub-tile of a query tile (m_used = -inf) takes
+// the exact path up front: tile max, then the weights.
+constexpr float kSumLimit = 65536.f;
+
+// p = 2^a for one block into P^T (bf16); returns the per-lane sum of the
+// rounded p.
+__device__ __forceinline__ float pack_sum(const f32x16& arg, bf16x8 (&pf)[2]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) pf[r >> 3][r & 7] = (__bf16)__builtin_amdgcn_exp2f(arg[r]);
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[0][2 * i], pf[0][2 * i + 1]}, one, a0, false);
+    a1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[1][2 * i], pf[1][2 * i + 1]}, one, a1, false);
+  }
+  return a0 + a1;
+}
+
+template <int D>
+__device__ __forceinline__ void softmax_pp(int lane, int valid, bool first, f32x16 (&sacc)[2][1],
+                                           bf16x8 (&pf)[2][2], f32x16 (&oacc)[2][D / 32], float (&m_used)[2],
+                                           float (&lsum)[2], const float (&c)[2]) {
+  if (valid < 32) {  // keys past the range end score -inf (see tile_max)
+    const int lim = valid - 4 * (lane >> 5);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (8 * (r >> 2) + (r & 3) >= lim) sacc[qb][0][r] = -INFINITY;
+  }
+  if (first) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) rescale<D>(oacc[qb], m_used[qb], lsum[qb], tile_max(lane, 32, sacc[qb], c[qb]));
+  }
+  // the arguments of both blocks first (independent), then one block at a
+  // time, so that a block's arguments die at its check
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[qb][0][r] = __builtin_fmaf(sacc[qb][0][r], c[qb], -m_used[qb]);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    float ts = pack_sum(sacc[qb][0], pf[qb]);
+    if (__any(!(ts <= kSumLimit))) {
+      float mx = 0.f;  // the shift: max(0, max a) over the row
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[qb][0][r]);
+      mx = max_halves(mx);
+      rescale<D>(oacc[qb], m_used[qb], lsum[qb], m_used[qb] + mx);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[qb][0][r] -= mx;
+      ts = pack_sum(sacc[qb][0], pf[qb]);
+    }
+    lsum[qb] += ts;
+  }
+}
+
 // V^T fragment f = cc * NB + nb of O^T += V^T P^T: two transpose reads of V
 // rows 16 cc + 4 (lane/32) + (lane%16)/4 (and 8 rows further) at
 // d = 32 nb + 16 ((lane/16)&1) + 4 (lane%4) .. +3, matching the key order of
-// P^T in the S^T accumulator.
+// P^T in the S^T accumulator.  Granule 4 nb + c = (4 nb) ^ c, so block nb is
+// the base XOR 64 nb bytes.
 template <int D>
-__device__ __forceinline__ bf16x8 v_frag(const uint16_t* vs, int lane, int f) {
-  constexpr int GR = D / 8;
+__device__ __forceinline__ bf16x8 v_frag(const uint16_t* vs, const FragBase& fb, int f) {
   constexpr int NB = D / 32;
   const int cc = f / NB, nb = f % NB;
-  const int hh = lane >> 5, li = lane & 15;
-  const int d = nb * 32 + ((lane >> 4) & 1) * 16 + 4 * (li & 3);
-  const int r0 = cc * 16 + 4 * hh + (li >> 2);
-  const int r1 = r0 + 8;
-  const uint16_t* a0p = vs + r0 * D + swz(r0, d >> 3, GR) * 8 + (d & 7);
-  const uint16_t* a1p = vs + r1 * D + swz(r1, d >> 3, GR) * 8 + (d & 7);
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0p));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1p));
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const char* base = reinterpret_cast<const char*>(vs) + cc * 16 * D * 2;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + (fb.v0 ^ uint32_t(64 * nb))));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + (fb.v1 ^ uint32_t(64 * nb))));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// O^T += V^T P^T for one 64-key tile: 16 keys per MFMA, 32 d-rows per MFMA.
-template <int D>
-__device__ __forceinline__ void pv_part(const uint16_t* vs, int lane, const bf16x8 (&pf)[4],
-                                        f32x16 (&oacc)[D / 32]) {
+// O^T += V^T P^T for sub-tile j: 16 keys per MFMA, 32 d-rows per MFMA.
+template <int D, int QB>
+__device__ __forceinline__ void pv_part(const uint16_t* vs, const FragBase& fb, int j,
+                                        const bf16x8 (&pf)[QB][2 * Blk<QB>::kKB], f32x16 (&oacc)[QB][D / 32]) {
   constexpr int NB = D / 32;
-  constexpr int NF = 4 * NB;
-  constexpr int PF = kPrefetch;
+  constexpr int NF = 2 * Blk<QB>::kKB * NB;
+  constexpr int PF = Blk<QB>::kPF;
   bf16x8 a[PF + 1];
 #pragma unroll
-  for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag<D>(vs, lane, f);
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag<D>(vs, fb, j * NF + f);
   sched_fence();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int cc = f / NB, nb = f % NB;
-    oacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], pf[cc], oacc[nb], 0, 0, 0);
-    if (f + PF < NF) a[(f + PF) % (PF + 1)] = v_frag<D>(vs, lane, f + PF);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+      oacc[qb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], pf[qb][cc], oacc[qb][nb], 0, 0, 0);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = v_frag<D>(vs, fb, j * NF + f + PF);
     sched_fence();
   }
 }
 
-// One 64-key tile for one wave: S^T = K Q^T, online softmax, O^T += V^T P^T.
-template <int D>
+// One 64-key tile for one wave, all phases back to back: per sub-tile
+// S^T = K Q^T, online softmax, O^T += V^T P^T.  A sub-tile wholly past the
+// range end is skipped (valid is wave-uniform).
+template <int D, int QB>
 __device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t* vs, int lane, int valid,
-                                             const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
-                                             float& lsum, float c) {
-  f32x16 sacc[2];
-  bf16x8 pf[4];
-  s_part<D>(ks, lane, qf, sacc);
-  softmax_part<D>(lane, valid, sacc, pf, oacc, m_used, lsum, c);
-  pv_part<D>(vs, lane, pf, oacc);
+                                             const bf16x8 (&qf)[QB][D / 16], f32x16 (&oacc)[QB][D / 32],
+                                             float (&m_used)[QB], float (&lsum)[QB], const float (&c)[QB]) {
+  constexpr int SUB = Blk<QB>::kSub, KB = Blk<QB>::kKB;
+#pragma unroll
+  for (int j = 0; j < kBN / SUB; ++j) {
+    if (j > 0 && valid <= j * SUB) break;
+    const FragBase fb = phase_base<D>(lane);
+    f32x16 sacc[QB][KB];
+    bf16x8 pf[QB][2 * KB];
+    s_part<D, QB>(ks, fb, j, qf, sacc);
+    softmax_part<D, QB>(lane, valid - j * SUB, sacc, pf, oacc, m_used, lsum, c);
+    pv_part<D, QB>(vs, fb, j, pf, oacc);
+  }
 }
 
 // ---------------------------------------------------------------- FP8 cache tiles
@@ -405,22 +582,34 @@ __device__ __forceinline__ int swz8(int row, int g) {
   return g ^ ((row / (256 / D)) & (D / 16 - 1));
 }
 
-// DMA of one FP8 tile: wave w < D/16 loads the 1 KB chunk w of K8 (into the
-// K8 stage `ks8`, swizzled) and of V8 (into V8 stage SV at byte 16 p,
-// unswizzled), lane l the 16-byte granule p = 64 w + l (row p / (D/16),
-// granule p % (D/16); cache rows are D bytes apart).  Rows past the range end
-// lie beyond the record count and arrive as zeros.
+// DMA of one FP8 tile: the 1 KB chunks w, w + kWaves, ... (of D/16 per
+// tensor) go to wave w; chunk ch of K8 lands in the K8 stage `ks8`
+// (swizzled), of V8 in V8 stage SV at byte 16 p (unswizzled), lane l taking
+// the 16-byte granule p = 64 ch + l (row p / (D/16), granule p % (D/16);
+// cache rows are D bytes apart).  Rows past the range end lie beyond the
+// record count and arrive as zeros.
+template <int D>
+constexpr int kChunks8 = kBN * (D / 16) / 64;
+// loads of one FP8 tile per loading wave (K8 and V8 of each chunk)
+template <int D>
+constexpr int kLoads8 = 2 * ((kChunks8<D> + kWaves - 1) / kWaves);
+
 template <int SV, int D>
 __device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, int lane, char* ks8) {
   constexpr int GR8 = D / 16;
-  constexpr int kChunks = kBN * GR8 / 64;
-  if (wave >= kChunks) return;
+  if (wave >= kChunks8<D>) return;
   const int nrec = min(kBN, c.rem) * D;
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
-  const int pos = wave * 64 + lane, row = pos / GR8, slot = pos % GR8;
-  dma16(lds_addr8(ks8 + wave * 1024), uint32_t(row * D + swz8<D>(row, slot) * 16), rk);
-  dma16(lds_addr8(v8buf<SV>() + wave * 1024), uint32_t(pos * 16), rv);
+#pragma unroll
+  for (int i = 0; i < (kChunks8<D> + kWaves - 1) / kWaves; ++i) {
+    const int ch = wave + i * kWaves;
+    if (ch < kChunks8<D>) {
+      const int pos = ch * 64 + lane, row = pos / GR8, slot = pos % GR8;
+      dma16(lds_addr8(ks8 + ch * 1024), uint32_t(row * D + swz8<D>(row, slot) * 16), rk);
+      dma16(lds_addr8(v8buf<SV>() + ch * 1024), uint32_t(pos * 16), rv);
+    }
+  }
 }
 
 // 16 codes (one 8-bit granule: d = 16 g .. 16 g + 15 of key row `row`) times
@@ -440,13 +629,16 @@ __device__ __forceinline__ void widen_granule(const char* src8, uint16_t* dst, i
   *reinterpret_cast<u32x4*>(dst + row * D + swz(row, 2 * g + 1, GR) * 8) = u32x4{e[4], e[5], e[6], e[7]};
 }
 
-// Widen V8 stage S into bf16 V stage S: thread i takes granule i (64 D / 16
-// granules: every thread at D = 128, the first half at D = 64).
+// Widen V8 stage S into bf16 V stage S: thread i takes granules i,
+// i + kThreads, ... (64 D / 16 granules).
 template <int S, int D>
 __device__ __forceinline__ void widen_v8(int tid, float sv) {
   constexpr int NG = kBN * (D / 16);
-  static_assert(NG <= kThreads, "one granule per thread");
-  if (NG == kThreads || tid < NG) widen_granule<D>(v8buf<S>(), vbuf<S>(), tid, sv);
+#pragma unroll
+  for (int g = 0; g < (NG + kThreads - 1) / kThreads; ++g) {
+    const int i = tid + g * kThreads;
+    if (NG % kThreads == 0 || i < NG) widen_granule<D>(v8buf<S>(), vbuf<S>(), i, sv);
+  }
 }
 
 // This lane's query row in e4m3 for the 8-bit QK^T: chunk c holds
@@ -472,24 +664,26 @@ __device__ __forceinline__ int e4m3_exponent(float amax) {
 template <int D>
 __device__ __forceinline__ int make_q8(const uint16_t* qrow, bool row_ok, int hh, Q8<D>& q8) {
   constexpr int NC = D / 64;
-  float x[NC][32];
+  // the row stays packed (two bf16 per register) and is unpacked per use
+  u32x4 raw[NC][4];
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const u32x4 raw = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * c + 32 * hh + 8 * g)
-                               : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        x[c][8 * g + 2 * w] = __uint_as_float(raw[w] << 16);
-        x[c][8 * g + 2 * w + 1] = __uint_as_float(raw[w] & 0xffff0000u);
-      }
-    }
-  float amax = 0.f;
+    for (int g = 0; g < 4; ++g)
+      raw[c][g] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * c + 32 * hh + 8 * g) : u32x4{0u, 0u, 0u, 0u};
+  const auto lo_half = [](uint32_t w) { return __uint_as_float(w << 16); };
+  const auto hi_half = [](uint32_t w) { return __uint_as_float(w & 0xffff0000u); };
+  // amax over the magnitude bits: for finite bf16 values the unsigned order of
+  // (bits & 0x7fff) is the order of |x|, so a packed 16-bit integer max finds it
+  u16x2 mx = {0, 0};
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
-    for (int i = 0; i < 32; ++i) amax = fmaxf(amax, fabsf(x[c][i]));
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, raw[c][g][w] & 0x7fff7fffu));
+  float amax = __uint_as_float(uint32_t(mx[0] > mx[1] ? mx[0] : mx[1]) << 16);
   amax = max_halves(amax);
   const int e = e4m3_exponent(amax);
   const float sc = ldexpf(1.f, -e);
@@ -497,8 +691,10 @@ __device__ __forceinline__ int make_q8(const uint16_t* qrow, bool row_ok, int hh
   for (int c = 0; c < NC; ++c)
 #pragma unroll
     for (int w = 0; w < 8; ++w) {
-      const float t0 = x[c][4 * w] * sc, t1 = x[c][4 * w + 1] * sc;
-      const float t2 = x[c][4 * w + 2] * sc, t3 = x[c][4 * w + 3] * sc;
+      // elements 4 w .. 4 w + 3 of the 32 this lane holds in chunk c
+      const uint32_t w0 = raw[c][w >> 1][2 * (w & 1)], w1 = raw[c][w >> 1][2 * (w & 1) + 1];
+      const float t0 = lo_half(w0) * sc, t1 = hi_half(w0) * sc;
+      const float t2 = lo_half(w1) * sc, t3 = hi_half(w1) * sc;
       int hi = __builtin_amdgcn_cvt_pk_fp8_f32(t0, t1, 0, false);
       hi = __builtin_amdgcn_cvt_pk_fp8_f32(t2, t3, hi, true);
       const auto b01 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false);
@@ -522,46 +718,51 @@ __device__ __forceinline__ i32x8 k8_frag(const char* ks8, int lane, int kb, int 
   return i32x8{int(a[0]), int(a[1]), int(a[2]), int(a[3]), int(b[0]), int(b[1]), int(b[2]), int(b[3])};
 }
 
-// S^T (in units of s_K 2^e) of one FP8 tile: per 32-key block and 64-wide
-// chunk of d, one 8-bit MFMA against hi (scale 1) and one against lo (scale
-// 2^-4), accumulating into the same registers.
-template <int D>
-__device__ __forceinline__ void s_part8(const char* ks8, int lane, const Q8<D>& q8, f32x16 (&sacc)[2]) {
+// S^T (in units of s_K 2^e) of sub-tile j of an FP8 tile for one query
+// block: per 32-key block and 64-wide chunk of d, one 8-bit MFMA against hi
+// (scale 1) and one against lo (scale 2^-4), accumulating into the same
+// registers.
+template <int D, int KB>
+__device__ __forceinline__ void s_part8(const char* ks8, int lane, int j, const Q8<D>& q8, f32x16 (&sacc)[KB]) {
   constexpr int NC = D / 64;
-  constexpr int NF = 2 * NC;
+  constexpr int NF = KB * NC;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
   i32x8 a[2];
-  a[0] = k8_frag<D>(ks8, lane, 0, 0);
+  a[0] = k8_frag<D>(ks8, lane, j * KB, 0);
   sched_fence();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int kb = f / NC, c = f % NC;
-    if (f + 1 < NF) a[(f + 1) & 1] = k8_frag<D>(ks8, lane, (f + 1) / NC, (f + 1) % NC);
+    if (f + 1 < NF) a[(f + 1) & 1] = k8_frag<D>(ks8, lane, j * KB + (f + 1) / NC, (f + 1) % NC);
     sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.hi[c], sacc[kb], 0, 0, 0, 127, 0, 127);
     sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.lo[c], sacc[kb], 0, 0, 0, 127, 0, 123);
     sched_fence();
   }
 }
 
-// Wait until at most `n` tiles of this wave's DMA loads are still in flight
-// (each tile is 2 * kLoads vector-memory instructions per wave).
-template <int kLoads>
+// ---------------------------------------------------------------- one-block ring
+// Every wave loads its share of each tile and computes it whole: per tile one
+// barrier, then the refill of the stage the previous tile freed, then the
+// tile's QK^T, softmax and PV.  Used with one query block per wave.
+
+// Wait until at most `n` tiles of this wave's loads are still in flight
+// (each tile is `per_tile` vector-memory instructions per wave).
+template <int per_tile>
 __device__ __forceinline__ void wait_tiles_in_flight(int n) {
-  static_assert(2 * kLoads * (kStages - 1) <= 63, "vmcnt range");
+  static_assert(2 * per_tile <= 63, "vmcnt range");
   if (n <= 0) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   } else if (n == 1) {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(per_tile) : "memory");
   } else {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * 2) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * per_tile) : "memory");
   }
 }
 
 // State a wave carries through the K/V ring.
-template <int D>
 struct RingState {
   Cursor icur, ccur;  // next tile to issue, next tile to compute
   int issued;         // tiles issued so far (absolute key-tile index)
@@ -569,14 +770,14 @@ struct RingState {
 
 // Tile k (in stage S): wait for its DMA, barrier, refill the stage that
 // became free with tile k + kStages - 1, then compute tile k.
-template <int S, int D>
+template <int S, int D, int QB>
 __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, int wave, int lane, bool wave_active,
-                                          const uint32_t* voff0, const uint32_t* voff1, RingState<D>& rs,
-                                          const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32], float& m_used,
-                                          float& lsum, float c) {
+                                          const uint32_t* voff0, const uint32_t* voff1, RingState& rs,
+                                          const bf16x8 (&qf)[QB][D / 16], f32x16 (&oacc)[QB][D / 32],
+                                          float (&m_used)[QB], float (&lsum)[QB], const float (&c)[QB]) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
   constexpr int F = (S + kStages - 1) % kStages;  // stage freed by the previous tile
-  wait_tiles_in_flight<kLoads>(rs.issued - 1 - k);
+  wait_tiles_in_flight<2 * kLoads>(rs.issued - 1 - k);
   ring_barrier();
   if (rs.issued < kt_end) {
     issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<F>(), vbuf<F>());
@@ -584,20 +785,21 @@ __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, in
     if (rs.issued < kt_end) cursor_next(p, rs.icur);
   }
   const int valid = tile_valid(rs.ccur);
-  if (wave_active) tile_compute<D>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
+  if (wave_active) tile_compute<D, QB>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
   if (k + 1 < kt_end) cursor_next(p, rs.ccur);
 }
 
 // The K/V ring over key tiles [kt_begin, kt_end) of query segment qs: tile kt
 // lives in stage (kt - kt_begin) % kStages; tiles up to kStages - 1 ahead are in
 // flight while one is computed.
-template <int D>
+template <int D, int QB>
 __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
                                          int wave, int lane, bool wave_active, const uint32_t* voff0,
-                                         const uint32_t* voff1, const bf16x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
-                                         float& m_used, float& lsum, float c) {
+                                         const uint32_t* voff1, const bf16x8 (&qf)[QB][D / 16],
+                                         f32x16 (&oacc)[QB][D / 32], float (&m_used)[QB], float (&lsum)[QB],
+                                         const float (&c)[QB]) {
   if (kt_begin >= kt_end) return;
-  RingState<D> rs;
+  RingState rs;
   rs.icur = cursor_at(p, qs, kt_begin, b, h);
   rs.ccur = rs.icur;
   rs.issued = kt_begin;
@@ -605,32 +807,205 @@ __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b,
     issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<0>(), vbuf<0>());
     if (++rs.issued < kt_end) cursor_next(p, rs.icur);
   }
-  if constexpr (kStages > 2) {
-    if (rs.issued < kt_end) {
-      issue_tile<D>(rs.icur, wave, voff0, voff1, kbuf<1>(), vbuf<1>());
-      if (++rs.issued < kt_end) cursor_next(p, rs.icur);
-    }
-  }
   for (int kt = kt_begin; kt < kt_end; kt += kStages) {
-    ring_step<0, D>(p, kt, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
+    ring_step<0, D, QB>(p, kt, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
     if (kt + 1 >= kt_end) break;
-    ring_step<1, D>(p, kt + 1, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
-    if constexpr (kStages > 2) {
-      if (kt + 2 >= kt_end) break;
-      ring_step<2, D>(p, kt + 2, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
-    }
+    ring_step<1, D, QB>(p, kt + 1, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
   }
 }
 
+// ---------------------------------------------------------------- ping-pong ring
+// With two query blocks per wave the two waves of each SIMD (waves w and w + 4
+// of the work-group share a SIMD) run half a phase apart: a wave alternates
+// an MFMA phase (P V of sub-tile u, then S^T of sub-tile u + 1) and a softmax
+// phase (sub-tile u + 1), with a work-group barrier between phases, and group
+// 1 (waves 4-7) starts one phase after group 0 (waves 0-3).  So while one
+// wave of a SIMD issues MFMAs the other one does its exp2/max/sum work, and
+// the two streams share the SIMD instead of taking turns.
+//
+// Group 1 alone loads the tiles (during its softmax phases), into a ring of
+// three stages: tile t + 2 is issued at the first softmax phase of tile t
+// (the stage of tile t - 1 is free by then for both groups), and group 1
+// waits for tile t + 1 at the end of the MFMA phase that precedes group 0's
+// first read of it.  Sub-tiles past the range end are computed with every
+// key masked, so that both groups pass the same barriers.
+constexpr int kLoaders = 4;  // waves of group 1
+
+// Issue the loads of one K/V tile from the loader wave lw of group 1: its
+// instruction i fills the 1 KB chunk c = i * 4 + lw of each tensor, lane l
+// the granule position p = 64 c + l (row p / (D/8), swizzled slot).
+template <int D>
+__device__ __forceinline__ void issue_tile_pp(const Cursor& c, int lw, int lane, uint16_t* ks, uint16_t* vs) {
+  constexpr int GR = D / 8;
+  constexpr int kLoads = kBN * GR / (kLoaders * 64);
+  const uint32_t nrec = uint32_t(min(kBN, c.rem)) * uint32_t(c.st);  // at most 2^31 (see issue_tile)
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
+  // the per-lane offsets are recomputed at every issue rather than kept live
+  asm volatile("" : "+v"(lane));
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) {
+    const int chunk = i * kLoaders + lw;
+    const int pos = chunk * 64 + lane;
+    const int row = pos / GR, slot = pos % GR;
+    const uint32_t voff =
+        uint32_t(row) * uint32_t(c.st) + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+    dma16(lds_addr(ks + chunk * 512), voff, rk);
+    dma16(lds_addr(vs + chunk * 512), voff, rv);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void wait_tiles_pp(int n) {
+  constexpr int kPerTile = 2 * (kBN * (D / 8) / (kLoaders * 64));
+  static_assert(2 * kPerTile <= 63, "vmcnt range");
+  if (n <= 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else if (n == 1) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPerTile) : "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kPerTile) : "memory");
+  }
+}
+
+// Pin a phase's results before the barrier that ends it: the empty asm
+// statement reads and rewrites the registers, so the compiler can neither sink
+// their computation into the next phase nor start it early.
+template <int QB, int KB>
+__device__ __forceinline__ void pin_scores(f32x16 (&sacc)[QB][KB]) {
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) asm volatile("" : "+v"(sacc[qb][kb]));
+}
+template <int QB, int N>
+__device__ __forceinline__ void pin_probs(bf16x8 (&pf)[QB][N], float (&m_used)[QB], float (&lsum)[QB]) {
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) asm volatile("" : "+v"(pf[qb][i]));
+    asm volatile("" : "+v"(m_used[qb]), "+v"(lsum[qb]));
+  }
+}
+
+struct PPState {
+  Cursor icur;  // next tile to load (group 1)
+  Cursor ccur;  // tile being computed
+  int issued;   // tiles loaded so far (group 1), counted from the first
+  int n;        // tiles of the range
+};
+
+// The four phases of tile t (stage S): softmax of sub-tile 2t, MFMA phase
+// (P V of 2t, S^T of 2t + 1), softmax of 2t + 1, MFMA phase (P V of 2t + 1,
+// S^T of sub-tile 0 of tile t + 1 in stage (S + 1) % 3).
+template <int S, int D>
+__device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int grp, int lw, int lane,
+                                        const bf16x8 (&qf)[2][D / 16], f32x16 (&oacc)[2][D / 32],
+                                        float (&m_used)[2], float (&lsum)[2], const float (&c)[2],
+                                        f32x16 (&sacc)[2][1], bf16x8 (&pf)[2][2]) {
+  constexpr int SN = (S + 1) % 3;  // stage of tile t + 1
+  constexpr int SL = (S + 2) % 3;  // stage of tile t - 1, refilled with tile t + 2
+  const int valid = tile_valid(st.ccur);
+  // softmax of sub-tile 2t; group 1 loads tile t + 2
+  ring_barrier();
+  if (grp == 1 && t >= 1 && t + 2 < st.n) {
+    issue_tile_pp<D>(st.icur, lw, lane, kbuf<SL>(), vbuf<SL>());
+    ++st.issued;
+    if (t + 3 < st.n) cursor_next(p, st.icur);
+  }
+  softmax_pp<D>(lane, valid, t == 0, sacc, pf, oacc, m_used, lsum, c);
+  pin_probs(pf, m_used, lsum);
+  // P V of sub-tile 2t, S^T of sub-tile 2t + 1; group 1 then waits for tile t + 1
+  ring_barrier();
+  {
+    const FragBase fb = phase_base<D>(lane);
+    pv_part<D, 2>(vbuf<S>(), fb, 0, pf, oacc);
+    s_part<D, 2>(kbuf<S>(), fb, 1, qf, sacc);
+    pin_scores(sacc);
+  }
+  if (grp == 1 && t + 1 < st.n) wait_tiles_pp<D>(st.issued - (t + 2));
+  // softmax of sub-tile 2t + 1
+  ring_barrier();
+  softmax_pp<D>(lane, valid - 32, false, sacc, pf, oacc, m_used, lsum, c);
+  pin_probs(pf, m_used, lsum);
+  // P V of sub-tile 2t + 1, S^T of the next tile's first sub-tile (after the
+  // last tile it reads a stage that holds no new tile and the scores go
+  // unused; computing it anyway keeps the old scores from living across this
+  // phase)
+  ring_barrier();
+  {
+    const FragBase fb = phase_base<D>(lane);
+    pv_part<D, 2>(vbuf<S>(), fb, 1, pf, oacc);
+    s_part<D, 2>(kbuf<SN>(), fb, 0, qf, sacc);
+    pin_scores(sacc);
+  }
+  if (t + 1 < st.n) cursor_next(p, st.ccur);
+}
+
+template <int D>
+__device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
+                                            int wave, int lane, const bf16x8 (&qf)[2][D / 16],
+                                            f32x16 (&oacc)[2][D / 32], float (&m_used)[2], float (&lsum)[2],
+                                            const float (&c)[2]) {
+  const int n = kt_end - kt_begin;  // the same for every wave of the work-group
+  if (n <= 0) return;
+  const int grp = wave >> 2, lw = wave & 3;
+  PPState st;
+  st.n = n;
+  st.ccur = cursor_at(p, qs, kt_begin, b, h);
+  st.icur = st.ccur;
+  st.issued = 0;
+  if (grp == 1) {
+    issue_tile_pp<D>(st.icur, lw, lane, kbuf<0>(), vbuf<0>());
+    st.issued = 1;
+    if (n > 1) {
+      cursor_next(p, st.icur);
+      issue_tile_pp<D>(st.icur, lw, lane, kbuf<1>(), vbuf<1>());
+      st.issued = 2;
+      if (n > 2) {
+        cursor_next(p, st.icur);
+        issue_tile_pp<D>(st.icur, lw, lane, kbuf<2>(), vbuf<2>());
+        st.issued = 3;
+        if (n > 3) cursor_next(p, st.icur);
+      }
+    }
+    wait_tiles_pp<D>(st.issued - 1);  // tile 0 landed
+  }
+  ring_barrier();
+  if (grp == 1) ring_barrier();  // group 1 runs one phase behind group 0
+  f32x16 sacc[2][1];
+  bf16x8 pf[2][2];
+  s_part<D, 2>(kbuf<0>(), phase_base<D>(lane), 0, qf, sacc);
+  pin_scores(sacc);
+  for (int t = 0; t < n; t += 3) {
+    pp_tile<0, D>(p, t, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+    if (t + 1 >= n) break;
+    pp_tile<1, D>(p, t + 1, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+    if (t + 2 >= n) break;
+    pp_tile<2, D>(p, t + 2, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+  }
+  if (grp == 0) ring_barrier();  // the barrier group 1 passed at the start
+}
+
+// ---------------------------------------------------------------- FP8 ring
 // Step j of n of the FP8 ring: wait for tile j + 1's loads, barrier (tile
 // j's widened V is visible; bf16 V stage (j + 1) % 2, V8 stage j % 2 and K8
 // stage (j + 2) % 3 are free), load tile j + 2, compute tile j, then widen
 // tile j + 1's V into bf16 stage (j + 1) % 2 (after the compute, so that the
-// tile's MFMAs start right after the barrier).
-template <int S, int D>
+// tile's MFMAs start right after the barrier).  Blocks take turns on the
+// 8-bit QK^T: a K8 fragment covers 64 d per MFMA, so the K side reads few
+// LDS bytes per MFMA and only the V^T fragments are shared.
+template <int S, int D, int QB>
 __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int tid, int wave, int lane,
-                                           bool wave_active, Cursor& icur, Cursor& ccur, float sv, const Q8<D>& q8,
-                                           f32x16 (&oacc)[D / 32], float& m_used, float& lsum, float cq) {
+                                           bool wave_active, Cursor& icur, Cursor& ccur, float sv,
+                                           const Q8<D> (&q8)[QB], f32x16 (&oacc)[QB][D / 32],
+                                           float (&m_used)[QB], float (&lsum)[QB], const float (&cq)[QB]) {
+  constexpr int SUB = Blk<QB>::kSub, KB = Blk<QB>::kKB;
+  // lane-derived LDS and buffer offsets are recomputed per tile instead of
+  // being kept live across the loop
+  asm volatile("" : "+v"(lane), "+v"(tid));
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   ring_barrier();
   if (j + 2 < n) {
@@ -639,11 +1014,20 @@ __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int ti
   }
   const int valid = tile_valid(ccur);
   if (wave_active) {
-    f32x16 sacc[2];
-    bf16x8 pf[4];
-    s_part8<D>(g_k8r[j % 3], lane, q8, sacc);
-    softmax_part<D>(lane, valid, sacc, pf, oacc, m_used, lsum, cq);
-    pv_part<D>(vbuf<S>(), lane, pf, oacc);
+#pragma unroll
+    for (int u = 0; u < kBN / SUB; ++u) {
+      if (u > 0 && valid <= u * SUB) break;
+      bf16x8 pf[QB][2 * KB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x16 sacc[KB];
+        s_part8<D, KB>(g_k8r[j % 3], lane, u, q8[qb], sacc);
+        const float mt = tile_max(lane, valid - u * SUB, sacc, cq[qb]);
+        if (__any(mt > m_used[qb] + kLazyThreshold)) rescale<D>(oacc[qb], m_used[qb], lsum[qb], mt);
+        exp_part(sacc, pf[qb], m_used[qb], lsum[qb], cq[qb]);
+      }
+      pv_part<D, QB>(vbuf<S>(), phase_base<D>(lane), u, pf, oacc);
+    }
   }
   if (j + 1 < n) widen_v8<S ^ 1, D>(tid, sv);
   if (j + 1 < n) cursor_next(p, ccur);
@@ -651,17 +1035,22 @@ __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int ti
 
 // The ring over FP8 cache tiles [kt_begin, kt_end): loads run two tiles
 // ahead of the compute, V widening one tile ahead.  qrow: this lane's query
-// row (bf16), read again here to build its e4m3 parts.
-template <int D>
+// row of each block (bf16), read again here to build its e4m3 parts.
+template <int D, int QB>
 __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
-                                          int tid, int wave, int lane, bool wave_active, const uint16_t* qrow,
-                                          bool row_ok, float sk, float sv, f32x16 (&oacc)[D / 32], float& m_used,
-                                          float& lsum, float c) {
+                                          int tid, int wave, int lane, bool wave_active,
+                                          const uint16_t* const (&qrow)[QB], const bool (&row_ok)[QB], float sk,
+                                          float sv, f32x16 (&oacc)[QB][D / 32], float (&m_used)[QB],
+                                          float (&lsum)[QB], float c) {
   const int n = kt_end - kt_begin;
   if (n <= 0) return;
-  Q8<D> q8;
-  const int e = make_q8<D>(qrow, row_ok, lane >> 5, q8);
-  const float cq = c * sk * ldexpf(1.f, e);  // scores are s_K 2^e times the accumulated ones
+  Q8<D> q8[QB];
+  float cq[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int e = make_q8<D>(qrow[qb], row_ok[qb], lane >> 5, q8[qb]);
+    cq[qb] = c * sk * ldexpf(1.f, e);  // scores are s_K 2^e times the accumulated ones
+  }
   Cursor icur = cursor_at(p, qs, kt_begin, b, h);
   Cursor ccur = icur;
   issue_tile8<0, D>(icur, wave, lane, g_k8r[0]);
@@ -669,17 +1058,17 @@ __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b
     cursor_next(p, icur);
     issue_tile8<1, D>(icur, wave, lane, g_k8r[1]);
     if (n > 2) cursor_next(p, icur);
-    // tile 0 landed, tile 1 (two loads per loading wave) may be in flight
-    asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    // tile 0 landed, tile 1 may be in flight
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoads8<D>) : "memory");
   } else {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
   ring_barrier();
   widen_v8<0, D>(tid, sv);
   for (int j = 0; j < n; j += 2) {
-    ring8_step<0, D>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
+    ring8_step<0, D, QB>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
     if (j + 1 >= n) break;
-    ring8_step<1, D>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
+    ring8_step<1, D, QB>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
   }
 }
 
@@ -695,51 +1084,43 @@ __device__ __forceinline__ int xcd_logical_block(int bid, int nblk) {
 // One query tile t of segment qs, batch b, head h, over the segment's key
 // tiles [kt_begin, kt_end).  part_row < 0: final output (bf16 O and LSE);
 // otherwise unnormalised fp32 partials (O, running max in log2 units, row
-// sum) at workspace row part_row + (row inside the tile).
-template <int D, bool kF8>
+// sum) at workspace row part_row + (row inside the tile).  Wave w owns rows
+// w * 32 QB .. + 32 QB - 1 of the tile, block qb of it rows
+// w * 32 QB + 32 qb + lane % 32.
+template <int D, bool kF8, int QB>
 __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int t, int b, int h, int kt_begin,
                                             int kt_end, int64_t part_row, int wave, int lane) {
   constexpr int GR = D / 8;
   constexpr int NDC = D / 16;  // 16-wide d chunks of the QK^T contraction
   constexpr int NB = D / 32;   // 32-wide d blocks of the output
   constexpr int kLoads = kBN * GR / kThreads;
+  constexpr int BM = Blk<QB>::kRows;
+  constexpr int RW = 32 * QB;  // query rows per wave
+  constexpr bool kPingPong = QB == 2 && !kF8;
   static_assert(kLoads >= 1 && kBN * GR % kThreads == 0, "tile granules must divide over the threads");
-  static_assert(kStages >= 2 && kStages <= 3, "stage ring of 2 or 3 tiles");
+  static_assert(!kPingPong || kWaves == 2 * kLoaders, "ping-pong pairs waves w and w + 4 on one SIMD");
   const int hh = lane >> 5;  // which 32-lane half
 
-  const int seg_row0 = (t - qs.tile0) * kBM;
-  const int rows_valid = min(kBM, qs.len - seg_row0);
+  const int seg_row0 = (t - qs.tile0) * BM;
+  const int rows_valid = min(BM, qs.len - seg_row0);
   const int row0 = qs.row0 + seg_row0;  // first row of the tile in the Q/O buffers
-  const bool wave_active = wave * 32 < rows_valid;  // wave-uniform
+  const bool wave_active = wave * RW < rows_valid;  // wave-uniform
 
-  // per-lane byte offsets of this lane's granules inside a tile, per key source
-  uint32_t voff0[kLoads], voff1[kLoads];
+  // ---- Q fragments (B operand of S^T = K Q^T): in block qb, lane holds
+  // query (lane % 32), d = 16*dc + 8*hh .. +7.
+  int my_row[QB];
+  bool row_ok[QB];
+  bf16x8 qf[QB][NDC];
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int pos = (i * kWaves + wave) * 64 + lane;
-    const int row = pos / GR, slot = pos % GR;
-    const uint32_t g16 = uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
-    voff0[i] = uint32_t(row) * uint32_t(p.src[0].k_st) + g16;
-    voff1[i] = uint32_t(row) * uint32_t(p.src[1].k_st) + g16;
-  }
-  // FP8 cache tiles: the scales of this (batch, head)
-  float sk = 1.f, sv = 1.f;
-  if constexpr (kF8) {
-    sk = p.kv_scale[(int64_t(b) * p.H + h) * 2];
-    sv = p.kv_scale[(int64_t(b) * p.H + h) * 2 + 1];
-  }
-
-  // ---- Q fragment (B operand of S^T = K Q^T): lane holds query (lane % 32),
-  // d = 16*dc + 8*hh .. +7.
-  const int my_row = wave * 32 + (lane & 31);
-  const bool row_ok = my_row < rows_valid;
-  bf16x8 qf[NDC];
-  {
-    const uint16_t* qp = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row) * p.q_st + int64_t(h) * D + hh * 8;
+  for (int qb = 0; qb < QB; ++qb) {
+    my_row[qb] = wave * RW + 32 * qb + (lane & 31);
+    row_ok[qb] = my_row[qb] < rows_valid;
+    const uint16_t* qp =
+        p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row[qb]) * p.q_st + int64_t(h) * D + hh * 8;
 #pragma unroll
     for (int dc = 0; dc < NDC; ++dc) {
-      u32x4 raw = row_ok ? *reinterpret_cast<const u32x4*>(qp + dc * 16) : u32x4{0u, 0u, 0u, 0u};
-      qf[dc] = __builtin_bit_cast(bf16x8, raw);
+      u32x4 raw = row_ok[qb] ? *reinterpret_cast<const u32x4*>(qp + dc * 16) : u32x4{0u, 0u, 0u, 0u};
+      qf[qb][dc] = __builtin_bit_cast(bf16x8, raw);
     }
   }
   // Q in registers before any tile DMA is counted; a compiler-visible wait
@@ -747,71 +1128,110 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
   // that no further waits for these loads are inserted inside the loop
   __builtin_amdgcn_s_waitcnt(0x0F70);
 
-  f32x16 oacc[NB];
+  f32x16 oacc[QB][NB];
+  float m_used[QB], lsum[QB], cb[QB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[nb][r] = 0.f;
-  float m_used = -INFINITY;  // running max in log2 units
-  float lsum = 0.f;          // this half's partial row sum
-  const float c = p.scale_log2;
-
-  if constexpr (kF8) {
-    // the planner puts this segment's fresh (bf16) key ranges before its FP8
-    // cache ranges: one ring over each kind
-    int kt_split = 0;
-    for (int r = qs.r0; r < qs.r0 + qs.nr && p.range[r].src == 0; ++r) kt_split += p.range[r].ntiles;
-    const int mid = min(max(kt_split, kt_begin), kt_end);
-    run_ring<D>(p, qs, b, h, kt_begin, mid, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c);
-    if (kt_begin < mid && mid < kt_end) ring_barrier();  // the first ring's stages are read no more
-    const uint16_t* qrow = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row) * p.q_st + int64_t(h) * D;
-    run_ring8<D>(p, qs, b, h, mid, kt_end, wave * 64 + lane, wave, lane, wave_active, qrow, row_ok, sk, sv, oacc,
-                 m_used, lsum, c);
-  } else {
-    run_ring<D>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, c);
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[qb][nb][r] = 0.f;
+    m_used[qb] = -INFINITY;  // running max in log2 units
+    lsum[qb] = 0.f;          // this half's partial row sum
+    cb[qb] = p.scale_log2;
   }
 
-  // ---- epilogue
-  const float l_tot = sum_halves(lsum);
-  if (!row_ok) return;
-  if (part_row >= 0) {
-    const int64_t prow = part_row + my_row;
-    float* op = p.ws_o + prow * D;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = nb * 32 + 8 * q4 + 4 * hh;
-        float4 v4 = make_float4(oacc[nb][4 * q4], oacc[nb][4 * q4 + 1], oacc[nb][4 * q4 + 2], oacc[nb][4 * q4 + 3]);
-        *reinterpret_cast<float4*>(op + d) = v4;
-      }
-    if (hh == 0) {
-      p.ws_ml[prow * 2] = m_used;
-      p.ws_ml[prow * 2 + 1] = l_tot;
-    }
+  if constexpr (kPingPong) {
+    // every wave computes (a wave past the tile's rows holds zero queries and
+    // stores nothing): keeping the phases unconditional lets the score and
+    // P registers die at each phase instead of living across the next one
+    run_ring_pp<D>(p, qs, b, h, kt_begin, kt_end, wave, lane, qf, oacc, m_used, lsum, cb);
   } else {
-    const int grow = row0 + my_row;
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(grow) * p.o_st + int64_t(h) * D;
+    // per-lane byte offsets of this lane's granules inside a tile, per key source
+    uint32_t voff0[kLoads], voff1[kLoads];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int i = 0; i < kLoads; ++i) {
+      const int pos = (i * kWaves + wave) * 64 + lane;
+      const int row = pos / GR, slot = pos % GR;
+      const uint32_t g16 = uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+      voff0[i] = uint32_t(row) * uint32_t(p.src[0].k_st) + g16;
+      voff1[i] = uint32_t(row) * uint32_t(p.src[1].k_st) + g16;
+    }
+    if constexpr (kF8) {
+      // the planner puts this segment's fresh (bf16) key ranges before its FP8
+      // cache ranges: one ring over each kind
+      int kt_split = 0;
+      for (int r = qs.r0; r < qs.r0 + qs.nr && p.range[r].src == 0; ++r) kt_split += p.range[r].ntiles;
+      const int mid = min(max(kt_split, kt_begin), kt_end);
+      run_ring<D, QB>(p, qs, b, h, kt_begin, mid, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum,
+                      cb);
+      if (mid < kt_end) {
+        if (kt_begin < mid) ring_barrier();  // the first ring's stages are read no more
+        // the scales of this (batch, head), read only when cache tiles exist
+        const float sk = p.kv_scale[(int64_t(b) * p.H + h) * 2];
+        const float sv = p.kv_scale[(int64_t(b) * p.H + h) * 2 + 1];
+        const uint16_t* qrow[QB];
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int d = nb * 32 + 8 * q4 + 4 * hh;
-        __bf16 o4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(oacc[nb][4 * q4 + j] * inv);
-        *reinterpret_cast<u32x2*>(op + d) = __builtin_bit_cast(u32x2, o4);
+        for (int qb = 0; qb < QB; ++qb)
+          qrow[qb] = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row[qb]) * p.q_st + int64_t(h) * D;
+        run_ring8<D, QB>(p, qs, b, h, mid, kt_end, wave * 64 + lane, wave, lane, wave_active, qrow, row_ok, sk, sv,
+                         oacc, m_used, lsum, p.scale_log2);
       }
-    if (p.lse && hh == 0)
-      p.lse[(int64_t(b) * p.H + h) * p.n_rows + grow] =
-          l_tot > 0.f ? m_used * 0.69314718055994531f + __logf(l_tot) : -INFINITY;
+    } else {
+      run_ring<D, QB>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum,
+                      cb);
+    }
+  }
+
+  // ---- epilogue (the half-sum exchange runs on every lane before any lane leaves)
+  float l_tot[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) l_tot[qb] = sum_halves(lsum[qb]);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    if (!row_ok[qb]) continue;
+    if (part_row >= 0) {
+      const int64_t prow = part_row + my_row[qb];
+      float* op = p.ws_o + prow * D;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = nb * 32 + 8 * q4 + 4 * hh;
+          float4 v4 = make_float4(oacc[qb][nb][4 * q4], oacc[qb][nb][4 * q4 + 1], oacc[qb][nb][4 * q4 + 2],
+                                  oacc[qb][nb][4 * q4 + 3]);
+          *reinterpret_cast<float4*>(op + d) = v4;
+        }
+      if (hh == 0) {
+        p.ws_ml[prow * 2] = m_used[qb];
+        p.ws_ml[prow * 2 + 1] = l_tot[qb];
+      }
+    } else {
+      const int grow = row0 + my_row[qb];
+      const float inv = l_tot[qb] > 0.f ? 1.f / l_tot[qb] : 0.f;
+      uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(grow) * p.o_st + int64_t(h) * D;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int d = nb * 32 + 8 * q4 + 4 * hh;
+          __bf16 o4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o4[j] = (__bf16)(oacc[qb][nb][4 * q4 + j] * inv);
+          *reinterpret_cast<u32x2*>(op + d) = __builtin_bit_cast(u32x2, o4);
+        }
+      if (p.lse && hh == 0)
+        p.lse[(int64_t(b) * p.H + h) * p.n_rows + grow] =
+            l_tot[qb] > 0.f ? m_used[qb] * 0.69314718055994531f + __logf(l_tot[qb]) : -INFINITY;
+    }
   }
 }
 
-// One work-group per (batch, head, query tile, key split).
+// One work-group per (batch, head, query tile, key split).  The host plans
+// the query tiles with p.bm = rows_per_wg of the kernel's block count.
 template <int D, bool kSplit, bool kF8>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
+  constexpr int QB = kF8 ? kQBFp8 : kQBPlain;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int w = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -828,8 +1248,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
   const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
   int64_t part_row = -1;
   if constexpr (kSplit)
-    part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * kBM;
-  attend_tile<D, kF8>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
+    part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * Blk<QB>::kRows;
+  attend_tile<D, kF8, QB>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
 }
 
 // Balanced schedule: work-group g of G takes the key-tile units
@@ -838,7 +1258,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(const Params p) {
 // written directly; a cut one leaves partials: the work-group's first piece
 // in workspace slot 2 g, its last piece (when not also its first) in 2 g + 1.
 template <int D, bool kF8>
-__global__ __launch_bounds__(kThreads) void attn_fwd_balanced_kernel(const Params p) {
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_balanced_kernel(const Params p) {
+  constexpr int QB = kQBBalanced;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -857,9 +1278,9 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_balanced_kernel(const Param
     const int kt0 = int(r - int64_t(tl) * qs.ktiles);
     const int kt1 = int(min(int64_t(qs.ktiles), int64_t(kt0) + (hi - u)));
     const bool whole = kt0 == 0 && kt1 == qs.ktiles;
-    const int64_t part_row = whole ? -1 : int64_t(first ? 2 * g : 2 * g + 1) * kBM;
+    const int64_t part_row = whole ? -1 : int64_t(first ? 2 * g : 2 * g + 1) * Blk<QB>::kRows;
     if (!first) ring_barrier();  // every wave is done with the previous piece's LDS stages
-    attend_tile<D, kF8>(p, qs, qs.tile0 + tl, int(bh / p.H), int(bh % p.H), kt0, kt1, part_row, wave, lane);
+    attend_tile<D, kF8, QB>(p, qs, qs.tile0 + tl, int(bh / p.H), int(bh % p.H), kt0, kt1, part_row, wave, lane);
     u += kt1 - kt0;
     first = false;
   }
@@ -883,7 +1304,7 @@ __global__ __launch_bounds__(256) void combine_balanced_kernel(const Params p, i
   int qi = 0;
   while (qi + 1 < p.n_qseg && p.qseg[qi + 1].row0 <= row) ++qi;
   const QSeg& qs = p.qseg[qi];
-  const int tl = (row - qs.row0) / kBM, rin = (row - qs.row0) % kBM;
+  const int tl = (row - qs.row0) / p.bm, rin = (row - qs.row0) % p.bm;
   uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(row) * p.o_st + int64_t(h) * D + 4 * d4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float M = -INFINITY, l = 0.f;
@@ -899,7 +1320,7 @@ __global__ __launch_bounds__(256) void combine_balanced_kernel(const Params p, i
       const int64_t lo = g * W / G;
       if (lo == (g + 1) * W / G) continue;
       const int64_t slot = (g == gf && lo < s) ? 2 * g + 1 : 2 * g;
-      const int64_t prow = slot * kBM + rin;
+      const int64_t prow = slot * p.bm + rin;
       if (p.ws_ml[prow * 2 + 1] > 0.f) M = fmaxf(M, p.ws_ml[prow * 2]);
     }
     if (M != -INFINITY) {
@@ -907,7 +1328,7 @@ __global__ __launch_bounds__(256) void combine_balanced_kernel(const Params p, i
         const int64_t lo = g * W / G;
         if (lo == (g + 1) * W / G) continue;
         const int64_t slot = (g == gf && lo < s) ? 2 * g + 1 : 2 * g;
-        const int64_t prow = slot * kBM + rin;
+        const int64_t prow = slot * p.bm + rin;
         const float ls = p.ws_ml[prow * 2 + 1];
         if (!(ls > 0.f)) continue;
         const float wgt = __builtin_amdgcn_exp2f(p.ws_ml[prow * 2] - M);

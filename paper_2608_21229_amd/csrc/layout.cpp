@@ -215,7 +215,7 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first) {
     s.nr = nr;
     s.ktiles = ktiles;
     s.unit0 = p.units_bh;
-    const int ntiles = (s.len + kBM - 1) / kBM;
+    const int ntiles = (s.len + p.bm - 1) / p.bm;
     p.n_qtiles += ntiles;
     p.units_bh += int64_t(ntiles) * ktiles;
   }
@@ -229,7 +229,7 @@ int32_t auto_splits(const Params& p) {
   // measured more than the idle CUs of a partial second round.  Keep >= 8 key
   // tiles per split.
   const int64_t wgs = int64_t(p.B) * p.H * p.n_qtiles;
-  const int64_t slots = 256 * (8 / kWaves);
+  const int64_t slots = 256;  // one work-group per CU
   if (wgs <= 0 || wgs >= slots) return 1;
   int max_kt = 0;
   for (int i = 0; i < p.n_qseg; ++i)

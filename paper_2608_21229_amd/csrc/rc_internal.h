@@ -16,15 +16,15 @@
 
 namespace rc {
 
-#ifndef RC_WAVES
-#define RC_WAVES 8                // waves per work-group, 32 query rows each
-#endif
-#ifndef RC_STAGES
-#define RC_STAGES 2               // K/V tiles resident in LDS (prefetch distance RC_STAGES - 1)
-#endif
-constexpr int kWaves = RC_WAVES;
-constexpr int kStages = RC_STAGES;
-constexpr int kBM = 32 * kWaves;  // query rows per work-group
+constexpr int kWaves = 8;         // waves per work-group (two per SIMD)
+constexpr int kStages = 2;        // K/V tiles resident in LDS in the one-block ring
+// 32-row query blocks per wave.  The bf16 kernels give each wave two blocks
+// (BM = 512 rows per work-group); the FP8-cache step and the balanced
+// schedule keep one (BM = 256), which their registers allow.
+constexpr int kQBPlain = 2;
+constexpr int kQBFp8 = 1;
+constexpr int kQBBalanced = 1;
+constexpr int rows_per_wg(int qb) { return 32 * qb * kWaves; }
 constexpr int kBN = 64;           // keys per K/V tile
 constexpr int kMaxRanges = 96;    // merged key ranges over all query segments
 constexpr int kMaxSplits = 32;
@@ -70,6 +70,7 @@ struct Params {
   float* ws_ml;        // split partials [splits, B, H, n_rows, 2] (max in log2 units, sum)
   KeySrc src[2];
   int32_t B, H, n_rows, n_qseg, n_qtiles, splits;  // splits: kSplitsBalanced = balanced schedule
+  int32_t bm;          // query rows per work-group tile (rows_per_wg of the kernel that runs)
   int32_t fp8;         // key source 1 is the FP8 cache
   const float* kv_scale;  // FP8 cache: [B, H, 2] power-of-two scales of K and V
   int64_t units_bh;    // key-tile units (query tile x key tile) per (batch, head)
@@ -140,7 +141,8 @@ rc_status check_layout(const rc_layout* L, int32_t entry);  // sets the thread e
 uint32_t cached_mask(const rc_layout* L);                  // bit i: segment i is cached
 int64_t count_rows(const rc_layout* L, RowSet set);
 int64_t count_cached_rows(const rc_layout* L);
-// Fill p.qseg / p.range / n_qseg / n_qtiles / n_rows for an entry.
+// Fill p.qseg / p.range / n_qseg / n_qtiles / n_rows for an entry, with
+// query tiles of p.bm rows (set by the caller).
 rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first = false);
 int32_t auto_splits(const Params& p);
 

@@ -206,14 +206,16 @@ def test_fragmented_schedule_is_refused():
 
 
 def test_auto_splits_and_workspace():
+    # 512-row query tiles: LT 512 is one tile, X 4096 eight, so 9 per head;
+    # the splits fill at most one round of 256 work-groups
     L = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
-    assert L.auto_splits(1, 24, 128) == 1            # 432 query tiles already exceed one round
+    assert L.auto_splits(1, 24, 128) == 1            # 216 query tiles: a second split would need two rounds
     assert L.workspace_bytes(1, 24, 128, 0) == 0
-    # one GPU's share of 24 heads over 8: 54 query tiles, 4 splits keep one round
-    assert L.auto_splits(1, 3, 128) == 4
-    assert L.workspace_bytes(1, 3, 128, 0) == 4 * 3 * 4608 * 130 * 4
-    assert L.auto_splits(1, 7, 128) == 2             # 126 query tiles
-    assert L.auto_splits(1, 1, 128) == 14            # 18 query tiles
+    # one GPU's share of 24 heads over 8: 27 query tiles, 9 splits keep one round
+    assert L.auto_splits(1, 3, 128) == 9
+    assert L.workspace_bytes(1, 3, 128, 0) == 9 * 3 * 4608 * 130 * 4
+    assert L.auto_splits(1, 7, 128) == 4             # 63 query tiles
+    assert L.auto_splits(1, 1, 128) == 28            # 9 query tiles (393 key tiles allow up to 49)
     # few key tiles cap the splits at one per 8 key tiles
     L2 = rc.Layout([(1, 64), (2, 64)], "perref")
     assert L2.auto_splits(1, 1, 128) == 1
