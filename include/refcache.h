@@ -70,6 +70,17 @@ extern "C" {
  * 2 * 256 * 256 * (D + 2) * 4 bytes whatever the problem size. */
 #define RC_SPLITS_BALANCED (-1)
 
+/* `splits` value of rc_step_masked_attention for the tail split: two key
+ * splits per query tile, a long one (the first f of its key tiles) and a short
+ * one (the rest).  The long pieces are dispatched first, one work-group per
+ * CU; the short ones run on the CUs the query tiles leave free, several in
+ * turn, so that both finish together: with Q query tiles (Q < 256) every CU
+ * but Q runs R = ceil(Q / (256 - Q)) short pieces and f = R / (R + 1).  The
+ * two partials of each row are merged in split order.  Workspace as for
+ * splits = 2.  rc_step_auto_splits returns it when the query tiles alone
+ * fill more than half the CUs and R <= 3 (Q <= 192). */
+#define RC_SPLITS_TAIL (-2)
+
 typedef enum {
   RC_OK = 0,
   RC_ERR_ARG = -1,                 /* null/misaligned pointer, bad size or stride */
@@ -142,11 +153,16 @@ int64_t rc_pairs(const rc_layout* L, int32_t entry);
 int64_t rc_rows(const rc_layout* L, int32_t which);
 
 /* Bytes of fp32 workspace rc_step_masked_attention needs for `splits`
- * key splits (0 when splits <= 1): splits * B * H * N_live * (D + 2) * 4.
- * splits = 0 resolves the automatic choice first.  0 on invalid input. */
+ * key splits (0 when splits == 1): splits * B * H * N_live * (D + 2) * 4,
+ * two splits' worth for RC_SPLITS_TAIL, and the fixed size given above for
+ * RC_SPLITS_BALANCED.  splits = 0 resolves the automatic choice first.
+ * 0 on invalid input. */
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits);
 
-/* The split count rc_step_masked_attention uses when passed splits = 0. */
+/* The split count rc_step_masked_attention uses when passed splits = 0: 1
+ * when the query tiles fill more than 192 CUs, RC_SPLITS_TAIL when they fill
+ * more than half, otherwise as many even splits as keep one round of work-groups (at
+ * most one per 8 key tiles and 32 in all). */
 int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D);
 
 /* Static-subgraph prefill (Sec. 3.3; App. C, Eq. cost-pre).
@@ -169,9 +185,11 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
  *   k_cache, v_cache        [B, H, N_cached, D] as written by rc_ref_kv_prefill.
  *   o_live                  [B, N_live, H, D] out;  lse_live [B, H, N_live] fp32, nullable.
  *   splits                  key splits per query tile (split-KV); 0 = automatic,
- *                           1 = none.  splits > 1 needs `workspace` (device,
- *                           16-byte aligned) of rc_step_workspace_bytes bytes;
- *                           partials are merged in a fixed order. */
+ *                           1 = none, 2..32 even splits, RC_SPLITS_TAIL,
+ *                           RC_SPLITS_BALANCED.  Anything but 1 needs
+ *                           `workspace` (device, 16-byte aligned) of
+ *                           rc_step_workspace_bytes bytes; partials are merged
+ *                           in a fixed order. */
 rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                    const void* q_live, const void* k_live, const void* v_live,
                                    int64_t tok_stride, const void* k_cache, const void* v_cache,

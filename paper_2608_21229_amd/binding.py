@@ -16,6 +16,7 @@ from typing import Iterable, Optional, Sequence, Tuple
 
 RC_MAX_SEGMENTS = 32
 SPLITS_BALANCED = -1   # rc_step_masked_attention: one round of 256 work-groups sharing all key tiles evenly
+SPLITS_TAIL = -2       # rc_step_masked_attention: a long and a short key split per query tile (idle CUs take the short)
 RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP = 0, -1, -2, -3, -4, -5
 SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
 MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE = 0, 1, 2, 3
@@ -188,6 +189,14 @@ def _inputs(q, k, v):
     return dev
 
 
+def _rows_of(layout: "Layout", q, which: int, what: str):
+    """The library sizes every read and write from the layout's row count, so
+    Q must hold exactly that many tokens (checked before anything else)."""
+    n = layout.rows(which)
+    if q.dim() != 4 or q.shape[1] != n:
+        raise ValueError(f"{what}: q must be [B, {n}, H, D] (the layout's row count), got {tuple(q.shape)}")
+
+
 def _same_device(dev, **tensors):
     for name, t in tensors.items():
         if t is not None and t.device != dev:
@@ -199,6 +208,7 @@ def ref_kv_prefill(layout: Layout, q, k, v, o=None, lse=None, k_cache=None, v_ca
     """Static-subgraph prefill.  q/k/v: [B, N_static, H, D] bf16 (ST and R
     tokens in sequence order).  Returns (o, lse or None, k_cache, v_cache)."""
     torch = _torch()
+    _rows_of(layout, q, ROWS_STATIC, "ref_kv_prefill")
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
@@ -228,8 +238,10 @@ def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse
                           workspace=None, scale: Optional[float] = None, want_lse: bool = False, stream=None):
     """Per-step attention.  q/k/v: [B, N_live, H, D] bf16 (LT and X tokens);
     k_cache/v_cache: [B, H, N_cached, D].  splits: 0 automatic, 1 none, > 1
-    split-KV, SPLITS_BALANCED the balanced schedule.  Returns (o, lse or None)."""
+    even split-KV, SPLITS_TAIL the tail split, SPLITS_BALANCED the balanced
+    schedule.  Returns (o, lse or None)."""
     torch = _torch()
+    _rows_of(layout, q, ROWS_LIVE, "step_masked_attention")
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
@@ -259,6 +271,7 @@ def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[fl
                    want_lse: bool = False, stream=None):
     """Full recompute over all rows.  q/k/v: [B, N, H, D] bf16.  Returns (o, lse or None)."""
     torch = _torch()
+    _rows_of(layout, q, ROWS_ALL, "full_attention")
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
@@ -323,6 +336,7 @@ def ref_kv_prefill_fp8(layout: Layout, q, k, v, o=None, lse=None, k_cache8=None,
     """Static-subgraph prefill writing the FP8 cache.  Returns
     (o, lse or None, k_cache8, v_cache8, kv_scale)."""
     torch = _torch()
+    _rows_of(layout, q, ROWS_STATIC, "ref_kv_prefill_fp8")
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale
@@ -357,6 +371,7 @@ def step_masked_attention_fp8(layout: Layout, q, k, v, k_cache8, v_cache8, kv_sc
     """Per-step attention reading the FP8 cache (fresh LT/X K/V stay bf16).
     Returns (o, lse or None)."""
     torch = _torch()
+    _rows_of(layout, q, ROWS_LIVE, "step_masked_attention_fp8")
     dev = _inputs(q, k, v)
     B, N, H, D = q.shape
     scale = 1.0 / math.sqrt(D) if scale is None else scale

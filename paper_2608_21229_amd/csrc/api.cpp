@@ -237,8 +237,9 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   RC_TRY(check_layout(L, RC_ENTRY_STEP));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
-  if (splits < kSplitsBalanced || splits > kMaxSplits) {
-    set_error("splits = %d must be RC_SPLITS_BALANCED (-1) or in [0, %d]", splits, kMaxSplits);
+  if (splits < kSplitsTail || splits > kMaxSplits) {
+    set_error("splits = %d must be RC_SPLITS_TAIL (-2), RC_SPLITS_BALANCED (-1) or in [0, %d]", splits,
+              kMaxSplits);
     return RC_ERR_ARG;
   }
   const int64_t n_live = count_rows(L, RowSet::Live);
@@ -281,7 +282,16 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   fill_common(p, B, H, scale);
   p.bm = rows_per_wg(fp8 ? kQBFp8 : balanced ? kQBBalanced : kQBPlain);
   RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
-  p.splits = splits;
+  if (splits == kSplitsTail) {
+    // the FP8 step tiles its queries by 256 rows: keep the tail split only
+    // where those tiles too fill more than half the CUs but not all
+    const int64_t q = int64_t(B) * H * p.n_qtiles;
+    p.splits = 2;
+    if (!fp8 || (2 * q > 256 && q < 256)) p.tail_num = tail_num(p);
+    else if (q >= 256) p.splits = 1;
+  } else {
+    p.splits = splits;
+  }
   if (balanced) {
     p.units = int64_t(B) * H * p.units_bh;
     p.bal_wgs = kBalancedWGs;
@@ -321,7 +331,7 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   CombineParams c;
   memset(&c, 0, sizeof c);
   if (p.splits > 1) {
-    const size_t need = size_t(p.splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);
+    const size_t need = rc_step_workspace_bytes(L, B, H, D, splits);
     if (!workspace || !aligned16(workspace) || ws_bytes < need) {
       set_error("split-KV with %d splits needs a 16-byte aligned workspace of %zu bytes (got %zu)", p.splits,
                 need, workspace ? ws_bytes : size_t(0));
@@ -385,9 +395,10 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
 
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
   if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
-  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsBalanced) return 0;
+  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsTail || splits > kMaxSplits) return 0;
   if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
   if (splits == kSplitsBalanced) return balanced_workspace_bytes(D);
+  if (splits == kSplitsTail) splits = 2;
   if (splits <= 1) return 0;
   const int64_t n_live = count_rows(L, RowSet::Live);
   return size_t(splits) * size_t(B) * size_t(H) * size_t(n_live) * size_t(D + 2) * sizeof(float);

@@ -1234,9 +1234,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   constexpr int QB = kF8 ? kQBFp8 : kQBPlain;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int w = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int split = w % p.splits;
-  int rest = w / p.splits;
+  int split, rest;
+  if (kSplit && p.tail_num > 0) {
+    // tail split: blocks [0, Q) are the long pieces, dispatched first; blocks
+    // [Q, 2 Q) the short ones.  Both halves map to query tiles the same way,
+    // so (for Q a multiple of 8) a tile's short piece runs on the XCD of its
+    // long piece, where the other short pieces of the head share its keys.
+    const int q = gridDim.x / 2;
+    split = blockIdx.x >= q;
+    rest = xcd_logical_block(blockIdx.x - split * q, q);
+  } else {
+    const int w = xcd_logical_block(blockIdx.x, gridDim.x);
+    split = w % p.splits;
+    rest = w / p.splits;
+  }
   const int t = rest % p.n_qtiles;
   rest /= p.n_qtiles;
   const int h = rest % p.H, b = rest / p.H;
@@ -1244,8 +1255,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   int qi = 0;
   while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
   const QSeg qs = p.qseg[qi];
-  const int kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
-  const int kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+  int kt_begin, kt_end;
+  if (kSplit && p.tail_num > 0) {
+    const int mid = int((int64_t(qs.ktiles) * p.tail_num) >> 10);
+    kt_begin = split ? mid : 0;
+    kt_end = split ? qs.ktiles : mid;
+  } else {
+    kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
+    kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
+  }
   int64_t part_row = -1;
   if constexpr (kSplit)
     part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * Blk<QB>::kRows;

@@ -223,22 +223,40 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first) {
 }
 
 int32_t auto_splits(const Params& p) {
-  // Split the keys only when the query tiles alone leave CUs idle, and only as
-  // far as one round of work-groups still fits on the 256 CUs: every extra
-  // split costs a Q load, a partial write and its share of the combine, which
-  // measured more than the idle CUs of a partial second round.  Keep >= 8 key
-  // tiles per split.
+  // Split the keys only when the query tiles alone leave CUs idle.  When they
+  // fill more than half of the 256 CUs, the tail split uses the rest: every
+  // query tile keeps one work-group for most of its keys and the short
+  // remainders run on the idle CUs, R = ceil(Q / (256 - Q)) in turn.  Each
+  // short piece pays a Q load, a partial write and its share of the combine,
+  // so beyond R = 3 (Q > 192) the split measured slower than none.  Below
+  // half, split evenly, as far as one round of work-groups still fits: a
+  // partial second round measured cheaper than the extra splits' overheads.
+  // Keep >= 8 key tiles per split.
   const int64_t wgs = int64_t(p.B) * p.H * p.n_qtiles;
   const int64_t slots = 256;  // one work-group per CU
   if (wgs <= 0 || wgs >= slots) return 1;
   int max_kt = 0;
   for (int i = 0; i < p.n_qseg; ++i)
     if (p.qseg[i].ktiles > max_kt) max_kt = p.qseg[i].ktiles;
+  if (2 * wgs > slots) {
+    const int64_t rounds = (wgs + (slots - wgs) - 1) / (slots - wgs);
+    return (rounds <= 3 && max_kt >= 16) ? kSplitsTail : 1;
+  }
   int64_t s = slots / wgs;
   const int64_t cap = max_kt / 8;
   if (s > cap) s = cap;
   if (s > kMaxSplits) s = kMaxSplits;
   return s < 1 ? 1 : int32_t(s);
+}
+
+int32_t tail_num(const Params& p) {
+  // Q query tiles on Q CUs; 256 - Q CUs run the short pieces, R rounds each:
+  // the long piece takes R / (R + 1) of the keys so both end together.
+  const int64_t q = int64_t(p.B) * p.H * p.n_qtiles;
+  const int64_t free_cus = 256 - q;
+  if (q <= 0 || free_cus <= 0) return 512;
+  const int64_t r = (q + free_cus - 1) / free_cus;
+  return int32_t(1024 * r / (r + 1));
 }
 
 }  // namespace rc

@@ -32,6 +32,7 @@ constexpr int kMaxSplits = 32;
 // each taking an equal contiguous share of all (query tile, key tile) units.
 constexpr int kBalancedWGs = 256;
 constexpr int32_t kSplitsBalanced = RC_SPLITS_BALANCED;
+constexpr int32_t kSplitsTail = RC_SPLITS_TAIL;
 
 struct KeyRange {
   int32_t start;   // first key token inside its source
@@ -71,6 +72,7 @@ struct Params {
   KeySrc src[2];
   int32_t B, H, n_rows, n_qseg, n_qtiles, splits;  // splits: kSplitsBalanced = balanced schedule
   int32_t bm;          // query rows per work-group tile (rows_per_wg of the kernel that runs)
+  int32_t tail_num;    // tail split (splits = 2): split 0 takes floor(ktiles * tail_num / 1024) key tiles; 0 = even
   int32_t fp8;         // key source 1 is the FP8 cache
   const float* kv_scale;  // FP8 cache: [B, H, 2] power-of-two scales of K and V
   int64_t units_bh;    // key-tile units (query tile x key tile) per (batch, head)
@@ -145,6 +147,7 @@ int64_t count_cached_rows(const rc_layout* L);
 // query tiles of p.bm rows (set by the caller).
 rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first = false);
 int32_t auto_splits(const Params& p);
+int32_t tail_num(const Params& p);  // the long split's share of the key tiles, in 1/1024
 
 void set_error(const char* fmt, ...);
 

@@ -127,13 +127,20 @@ def test_argument_errors_launch_nothing():
         assert fn(L, scale=float("nan")) == A
         assert fn(L, ts=2 * 128 - 8) == A              # token stride below H*D
         assert fn(L, ts=2 * 128 + 4) == A              # not a multiple of 8
-        assert fn(L, ts=(1 << 24) + 8) == A            # tile byte offsets would overflow 32 bits
+        assert fn(L, ts=(1 << 24) + 8) == A            # a tile's byte record count would pass 2^31
+        assert "tok_stride" in rc.lib().rc_last_error().decode()
+        # the largest stride passes its check (64 tokens x 2^25 bytes = 2^31
+        # fits the unsigned 32-bit record count); the call then fails on q
+        assert fn(L, ts=1 << 24, q=None) == A
+        assert "null" in rc.lib().rc_last_error().decode()
         assert fn(L, lse=FAKE + 2) == A                # misaligned LSE
         assert rc.lib().rc_last_error().decode() != ""
     assert _prefill(L, kc=None) == A
     assert _step(L, vc=None) == A
-    assert _step(L, splits=-2) == A
+    assert _step(L, splits=-3) == A
     assert _step(L, splits=33) == A
+    assert _step(L, splits=-2) == W                    # tail split, no workspace
+    assert L.workspace_bytes(1, 2, 128, -2) == L.workspace_bytes(1, 2, 128, 2)
     assert _step(L, splits=-1) == W                    # balanced schedule, no workspace
     need_bal = L.workspace_bytes(1, 2, 128, -1)
     assert need_bal == 2 * 256 * 256 * 130 * 4         # fixed: two partial tiles per work-group
@@ -209,8 +216,15 @@ def test_auto_splits_and_workspace():
     # 512-row query tiles: LT 512 is one tile, X 4096 eight, so 9 per head;
     # the splits fill at most one round of 256 work-groups
     L = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
-    assert L.auto_splits(1, 24, 128) == 1            # 216 query tiles: a second split would need two rounds
+    # 216 query tiles leave 40 CUs: their short pieces would take 6 rounds, no split
+    assert L.auto_splits(1, 24, 128) == 1
     assert L.workspace_bytes(1, 24, 128, 0) == 0
+    assert L.auto_splits(1, 22, 128) == 1            # 198 tiles: 4 rounds on 58 CUs
+    assert L.auto_splits(1, 21, 128) == rc.SPLITS_TAIL   # 189 tiles: 3 rounds on 67 CUs
+    assert L.workspace_bytes(1, 21, 128, 0) == 2 * 21 * 4608 * 130 * 4
+    assert L.auto_splits(1, 29, 128) == 1            # 261 query tiles fill every CU
+    assert L.auto_splits(1, 15, 128) == rc.SPLITS_TAIL   # 135 query tiles: more than half
+    assert L.auto_splits(1, 14, 128) == 2            # 126 query tiles: two even splits keep one round
     # one GPU's share of 24 heads over 8: 27 query tiles, 9 splits keep one round
     assert L.auto_splits(1, 3, 128) == 9
     assert L.workspace_bytes(1, 3, 128, 0) == 9 * 3 * 4608 * 130 * 4
@@ -221,16 +235,33 @@ def test_auto_splits_and_workspace():
     assert L2.auto_splits(1, 1, 128) == 1
 
 
+def test_binding_checks_row_counts():
+    """Every read and write is sized from the layout's row count, so the
+    binding refuses Q with another token count before anything else (no GPU
+    needed: the check comes before the device check)."""
+    import torch
+    L = rc.Layout([(0, 8), (1, 16), (2, 64), (3, 64)], "perref")   # 72 static, 80 live, 152 rows
+    cases = ((rc.ref_kv_prefill, 72), (rc.step_masked_attention, 80), (rc.full_attention, 152),
+             (rc.ref_kv_prefill_fp8, 72), (rc.step_masked_attention_fp8, 80))
+    for fn, n in cases:
+        for bad in (n - 1, n + 1):
+            q = torch.zeros(1, bad, 2, 64, dtype=torch.bfloat16)
+            args = (L, q, q, q) + ((None, None) if fn is rc.step_masked_attention else
+                                   (None, None, None) if fn is rc.step_masked_attention_fp8 else ())
+            with pytest.raises(ValueError, match=f"\\[B, {n}, H, D\\]"):
+                fn(*args)
+
+
 def test_binding_rejects_host_tensors():
     """The library takes raw device pointers: the binding refuses host tensors
     (and mismatched shapes) before any call into it."""
     import pytest
     import torch
     L = rc.Layout([(0, 8), (1, 16), (2, 64), (3, 64)], "perref")
-    q = torch.zeros(1, 72, 2, 64, dtype=torch.bfloat16)
-    for fn in (lambda: rc.ref_kv_prefill(L, q, q, q),
-               lambda: rc.full_attention(L, q, q, q),
-               lambda: rc.step_masked_attention(L, q, q, q, None, None)):
+    qs, ql, qa = (torch.zeros(1, n, 2, 64, dtype=torch.bfloat16) for n in (72, 80, 152))
+    for fn in (lambda: rc.ref_kv_prefill(L, qs, qs, qs),
+               lambda: rc.full_attention(L, qa, qa, qa),
+               lambda: rc.step_masked_attention(L, ql, ql, ql, None, None)):
         with pytest.raises(ValueError, match="GPU tensor"):
             fn()
 

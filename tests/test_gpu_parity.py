@@ -103,7 +103,7 @@ RAGGED = [
 def test_ragged_segments(name, segs, preset, D):
     from synthgen import Workload
     wl = Workload(f"{name}_D{D}", 2, 3, D, tuple(segs), std=1.0, seed=11)
-    for splits in (1, 3, 0, rc.SPLITS_BALANCED):
+    for splits in (1, 3, 0, rc.SPLITS_TAIL, rc.SPLITS_BALANCED):
         check_request(wl, preset, splits=splits)
 
 
@@ -228,7 +228,7 @@ def test_mixed48_layers(layer):
     check_request(workload("mixed48"), "perref", every=53, layer=layer, steps=(0, 19, 39))
 
 
-@pytest.mark.parametrize("splits", [1, 2, 4, 7, 0, -1])
+@pytest.mark.parametrize("splits", [1, 2, 4, 7, 0, rc.SPLITS_TAIL, rc.SPLITS_BALANCED])
 def test_split_kv_one_gpu_share(splits):
     """Headline shape at one GPU's share of heads (3 of 24): few query tiles,
     so split-KV carries the occupancy."""
