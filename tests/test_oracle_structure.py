@@ -74,6 +74,18 @@ def test_printed_large_context_approximation():
     assert oc.speedup(4096, 64, 4608, 40) > 1.8
 
 
+def test_speedup_worked_values():
+    """Eq. speedup at N_ST = 64, S = 4608, T = 40 with 1, 5 and 10 references
+    of 4096 tokens, against values worked by hand from the equation's integer
+    terms (the fixture's comments show each term)."""
+    g = read_golden_kv("cost_model.txt")
+    for k, key in [(1, "speedup_1ref_4dp"), (5, "speedup_5ref_4dp"), (10, "speedup_10ref_4dp")]:
+        val = oc.speedup(k * g["speedup_NR_per_ref"], g["speedup_n_st"], g["speedup_S"], g["speedup_T"])
+        assert round(val, 4) == g[key]
+        # the exact model stays below the large-context form's ceiling T
+        assert val < g["speedup_T"]
+
+
 def test_speedup_equation_consistency():
     # Eq. speedup written as C_full / C_ours with hand-expanded terms
     for n_r, n_st, s, T in [(4096, 64, 4608, 40), (20480, 64, 4608, 40), (1, 0, 1, 3)]:
