@@ -50,6 +50,8 @@ def layout_for(inp, preset):
 
 def check_request(wl, preset, every=None, splits=0, layer=0, steps=(0,)):
     """Prefill + steps for one layer; compare prefill O/LSE, cache bits, step O/LSE."""
+    print(f"[case] {wl.name}/{preset} B={wl.B} H={wl.H} D={wl.D} layer={layer} splits={splits} steps={steps}",
+          flush=True)
     inp0 = draw_inputs(wl, layer=layer, step=steps[0])
     L = layout_for(inp0, preset)
     vis = oracle_mask(inp0, preset)
@@ -139,7 +141,14 @@ def test_ref1_request_40_steps():
 
 @pytest.mark.parametrize("preset", ["perref", "paper"])
 def test_ref5_headline(preset):
-    check_request(workload("ref5"), preset, every=37)
+    """The 5-reference workload: first, middle and last of the 40 steps."""
+    check_request(workload("ref5"), preset, every=37, steps=(0, 19, 39))
+
+
+def test_ref1_paper_mask():
+    """The figure's mask (references see only their own block and the
+    anchors) at the single-reference shape, steps 0, 19 and 39."""
+    check_request(workload("ref1"), "paper", every=13, steps=(0, 19, 39))
 
 
 def test_ref5_isolated_cache():
@@ -223,9 +232,19 @@ def test_reference_scaling(k):
     check_request(workload(f"scaling_k{k}"), "perref", every=61)
 
 
+def test_reference_scaling_paper_mask_k10():
+    """Ten references under the figure's mask."""
+    check_request(workload("scaling_k10"), "paper", every=61, steps=(0, 39))
+
+
 @pytest.mark.parametrize("layer", [0, 23, 47])
 def test_mixed48_layers(layer):
     check_request(workload("mixed48"), "perref", every=53, layer=layer, steps=(0, 19, 39))
+
+
+@pytest.mark.parametrize("layer", [0, 47])
+def test_mixed48_layers_paper_mask(layer):
+    check_request(workload("mixed48"), "paper", every=53, layer=layer, steps=(0, 19, 39))
 
 
 @pytest.mark.parametrize("splits", [1, 2, 4, 7, 0, rc.SPLITS_TAIL, rc.SPLITS_BALANCED])
