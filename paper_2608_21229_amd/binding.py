@@ -24,7 +24,10 @@ ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL = 0, 1, 2
 ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL = 0, 1, 2, 3
 MASKS = {"paper": MASK_PAPER, "perref": MASK_PERREF, "isolated": MASK_ISOLATED, "dense": MASK_DENSE}
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librefcache.so")
+# REFCACHE_LIB names another build of the same ABI (the host tests load a
+# sanitizer build of the planner through it); by default the in-tree library.
+LIB_PATH = os.environ.get("REFCACHE_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                          "librefcache.so")
 
 
 class RcError(RuntimeError):
