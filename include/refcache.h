@@ -247,6 +247,29 @@ rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H,
 rc_status rc_linear(int64_t M, int32_t N, int32_t K, const void* a, int64_t lda, const void* w,
                     const void* r, int64_t ldr, void* out, int64_t ldo, void* stream);
 
+/* Bytes of the static device array (per GPU) behind
+ * rc_step_masked_attention_noalloc: 128 MiB, enough for the balanced schedule
+ * at D = 128 (65 MiB) and for two splits over 24 heads x 4608 live rows. */
+#define RC_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * rc_step_masked_attention with its split partials in a static device array
+ * of RC_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on,
+ * from that GPU's first call until the process ends.  Allocates nothing and
+ * calls no allocating routine.  Arguments, layouts and results as for
+ * rc_step_masked_attention, on the current device; the caller still owns and
+ * passes the inputs and outputs.  A split choice whose workspace
+ * (rc_step_workspace_bytes) exceeds RC_NOALLOC_SCRATCH_BYTES returns
+ * RC_ERR_WORKSPACE.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (several streams or host threads) race, so
+ * serialise them.  The array's earlier contents never matter (every partial
+ * a merge reads is written by the same call). */
+rc_status rc_step_masked_attention_noalloc(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                           const void* q_live, const void* k_live, const void* v_live,
+                                           int64_t tok_stride, const void* k_cache, const void* v_cache,
+                                           void* o_live, float* lse_live, int32_t splits, void* stream);
+
 /* Static description of a status code. */
 const char* rc_status_string(rc_status s);
 

@@ -10,7 +10,8 @@ drives a stack of synthetic layers (projection, attention, projection plus
 residual) through it.
 """
 from .binding import (  # noqa: F401
-    Layout, RcError, lib, ref_kv_prefill, step_masked_attention, full_attention, linear,
+    Layout, RcError, lib, ref_kv_prefill, step_masked_attention, step_masked_attention_noalloc, full_attention,
+    linear, NOALLOC_SCRATCH_BYTES,
     ref_kv_prefill_fp8, step_masked_attention_fp8, fp8_cache_shapes,
     SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF,
     MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE, MASKS,

@@ -16,6 +16,7 @@ from typing import Iterable, Optional, Sequence, Tuple
 
 RC_MAX_SEGMENTS = 32
 SPLITS_BALANCED = -1   # rc_step_masked_attention: one round of 256 work-groups sharing all key tiles evenly
+NOALLOC_SCRATCH_BYTES = 128 << 20   # rc_step_masked_attention_noalloc's static scratch per GPU
 SPLITS_TAIL = -2       # rc_step_masked_attention: a long and a short key split per query tile (idle CUs take the short)
 RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP = 0, -1, -2, -3, -4, -5
 SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
@@ -65,6 +66,8 @@ SIGNATURES = {
                                      _vp]),
     "rc_step_masked_attention_fp8": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                             _vp, _i32, _vp, _sz, _vp]),
+    "rc_step_masked_attention_noalloc": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
+                                                _vp, _i32, _vp]),
     "rc_status_string": (ctypes.c_char_p, [_i32]),
     "rc_last_error": (ctypes.c_char_p, []),
 }
@@ -267,6 +270,34 @@ def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse
                                               k.data_ptr(), v.data_ptr(), ts, _ptr(k_cache), _ptr(v_cache),
                                               o.data_ptr(), _ptr(lse), splits,
                                               _ptr(workspace) if need else None, need, _stream(stream, dev)))
+    return o, lse
+
+
+def step_masked_attention_noalloc(layout: Layout, q, k, v, k_cache, v_cache, o, lse=None, splits: int = 0,
+                                  scale: Optional[float] = None, stream=None):
+    """step_masked_attention without any device allocation: the caller passes
+    the output `o` (and `lse`, or None), and split partials go to the
+    library's static scratch array (NOALLOC_SCRATCH_BYTES per GPU; a larger
+    split choice raises RcError with RC_ERR_WORKSPACE).  Calls that overlap on
+    one GPU share that array and race.  Returns (o, lse)."""
+    if o is None:
+        raise ValueError("step_masked_attention_noalloc: pass the output o (it allocates nothing)")
+    _rows_of(layout, q, ROWS_LIVE, "step_masked_attention_noalloc")
+    dev = _inputs(q, k, v)
+    B, N, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    ts = _tok_stride(q, k, v)
+    nc = layout.rows(ROWS_CACHED)
+    _expect(o, (B, N, H, D), "torch.bfloat16", "o")
+    _expect(lse, (B, H, N), "torch.float32", "lse")
+    _expect(k_cache, (B, H, nc, D), "torch.bfloat16", "k_cache")
+    _expect(v_cache, (B, H, nc, D), "torch.bfloat16", "v_cache")
+    _same_device(dev, o=o, lse=lse, k_cache=k_cache, v_cache=v_cache)
+    with _torch().cuda.device(dev):
+        _check(lib().rc_step_masked_attention_noalloc(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(),
+                                                      k.data_ptr(), v.data_ptr(), ts, _ptr(k_cache),
+                                                      _ptr(v_cache), o.data_ptr(), _ptr(lse), splits,
+                                                      _stream(stream, dev)))
     return o, lse
 
 

@@ -413,6 +413,25 @@ rc_status rc_step_masked_attention(const rc_layout* L, int32_t B, int32_t H, int
                    lse_live, splits, workspace, ws_bytes, stream);
 }
 
+rc_status rc_step_masked_attention_noalloc(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                                           const void* q_live, const void* k_live, const void* v_live,
+                                           int64_t tok_stride, const void* k_cache, const void* v_cache,
+                                           void* o_live, float* lse_live, int32_t splits, void* stream) {
+  using namespace rc;
+  // the workspace the split choice needs (0 for none, or for invalid input,
+  // which step_impl then reports)
+  const size_t need = rc_step_workspace_bytes(L, B, H, D, splits);
+  if (need > size_t(RC_NOALLOC_SCRATCH_BYTES)) {
+    set_error("the no-allocation step holds %zu bytes of scratch; splits = %d needs %zu",
+              size_t(RC_NOALLOC_SCRATCH_BYTES), splits, need);
+    return RC_ERR_WORKSPACE;
+  }
+  void* ws = nullptr;
+  if (need > 0) RC_TRY(hip_status(scratch_address(&ws), "scratch lookup"));
+  return step_impl(L, B, H, D, scale, q_live, k_live, v_live, tok_stride, false, k_cache, v_cache, nullptr, o_live,
+                   lse_live, splits, ws, need > 0 ? size_t(RC_NOALLOC_SCRATCH_BYTES) : 0, stream);
+}
+
 rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
                                        const void* q_live, const void* k_live, const void* v_live,
                                        int64_t tok_stride, const void* k_cache8, const void* v_cache8,

@@ -43,6 +43,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "rc_internal.h"
 
 namespace rc {
@@ -1433,6 +1435,33 @@ template <int D, bool kF8>
 void launch_grid(const Params& p, int64_t blocks, hipStream_t s) {
   if (p.splits > 1) hipLaunchKernelGGL((attn_fwd_kernel<D, true, kF8>), dim3(blocks), dim3(kThreads), 0, s, p);
   else hipLaunchKernelGGL((attn_fwd_kernel<D, false, kF8>), dim3(blocks), dim3(kThreads), 0, s, p);
+}
+
+// Split partials of the no-allocation step entry.  In host code `scratch`
+// names a host-side stand-in: kernels get the device address that
+// scratch_address looks up once per device.
+static __device__ __align__(256) unsigned char scratch[RC_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+int scratch_address(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return int(e);
+  if (dev < 0 || dev >= kMaxDevices) return int(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return int(e);
+    g_scratch_ptr[dev] = a;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return int(hipSuccess);
 }
 
 int launch_attention(const Params& p, int D, void* stream) {

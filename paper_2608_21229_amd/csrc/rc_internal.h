@@ -159,5 +159,8 @@ int launch_combine_balanced(const Params& p, int D, void* stream);
 int launch_cache_store(const CacheStoreParams& c, void* stream);
 int launch_cache_store_fp8(const CacheStore8Params& c, void* stream);
 int launch_linear(const LinearParams& q, void* stream);  // linear.hip
+// Device address of the current GPU's static scratch array
+// (RC_NOALLOC_SCRATCH_BYTES), looked up once per device.  hipError_t as int.
+int scratch_address(void** ptr);
 
 }  // namespace rc

@@ -147,6 +147,13 @@ int launch_linear(const LinearParams& q, void*) {
   return 0;
 }
 
+// a fake, never dereferenced device address of the scratch array
+int scratch_address(void** ptr) {
+  *ptr = reinterpret_cast<void*>(uintptr_t(0x7f0000100000));
+  ++g_launches;
+  return 0;
+}
+
 }  // namespace rc
 
 extern "C" long rc_stub_launches(void) { return g_launches; }
