@@ -165,6 +165,18 @@ size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t
  * most one per 8 key tiles and 32 in all). */
 int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D);
 
+/* Launch shape of the step's attention kernel for `splits` (0 = automatic)
+ * with the bf16 cache (fp8 = 0) or the FP8 cache (fp8 = 1), for occupancy
+ * reports: *work_groups over all its launches (one per query tile and split;
+ * 256 for RC_SPLITS_BALANCED), *rows_per_wg the query rows per work-group,
+ * *splits_used the split count it resolves to (2 for the tail split, 1 where
+ * the FP8 step drops it, RC_SPLITS_BALANCED for the balanced schedule).
+ * Host only; RC_ERR_ARG on bad arguments or null outputs, RC_ERR_UNSUPPORTED
+ * for head_dim other than 64/128 and for the balanced schedule with the FP8
+ * cache. */
+rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits, int32_t fp8,
+                               int64_t* work_groups, int32_t* rows_per_wg, int32_t* splits_used);
+
 /* Static-subgraph prefill (Sec. 3.3; App. C, Eq. cost-pre).
  *   q_static, k_static, v_static  [B, N_static, H, D]: the ST and R tokens in
  *                                 sequence order (RC_ROWS_STATIC rows).

@@ -68,6 +68,8 @@ SIGNATURES = {
                                             _vp, _i32, _vp, _sz, _vp]),
     "rc_step_masked_attention_noalloc": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp,
                                                 _vp, _i32, _vp]),
+    "rc_step_launch_shape": (_i32, [_PL, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64),
+                                    ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
     "rc_status_string": (ctypes.c_char_p, [_i32]),
     "rc_last_error": (ctypes.c_char_p, []),
 }
@@ -140,6 +142,14 @@ class Layout:
 
     def workspace_bytes(self, B: int, H: int, D: int, splits: int = 0) -> int:
         return int(lib().rc_step_workspace_bytes(ctypes.byref(self.c), B, H, D, splits))
+
+    def launch_shape(self, B: int, H: int, D: int, splits: int = 0, fp8: bool = False):
+        """(work-groups, query rows per work-group, resolved splits) of the
+        step's attention kernel."""
+        wg, bm, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().rc_step_launch_shape(ctypes.byref(self.c), B, H, D, splits, int(fp8), ctypes.byref(wg),
+                                          ctypes.byref(bm), ctypes.byref(sp)))
+        return wg.value, bm.value, sp.value
 
     def auto_splits(self, B: int, H: int, D: int) -> int:
         return int(lib().rc_step_auto_splits(ctypes.byref(self.c), B, H, D))

@@ -228,6 +228,33 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
   return RC_OK;
 }
 
+// The step's schedule for a split choice (0 = automatic): query tiles, key
+// ranges and the resolved split count, in p (p.B and p.H set by the caller).
+rc_status plan_step(const rc_layout* L, int32_t D, bool fp8, int32_t splits, Params& p) {
+  // the automatic choice is the one rc_step_auto_splits reports (for either
+  // cache format)
+  if (splits == 0) splits = rc_step_auto_splits(L, p.B, p.H, D);
+  const bool balanced = splits == kSplitsBalanced;
+  p.bm = rows_per_wg(fp8 ? kQBFp8 : balanced ? kQBBalanced : kQBPlain);
+  RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
+  if (splits == kSplitsTail) {
+    // the FP8 step tiles its queries by 256 rows: keep the tail split only
+    // where those tiles too fill more than half the CUs but not all
+    const int64_t q = int64_t(p.B) * p.H * p.n_qtiles;
+    p.splits = 2;
+    if (!fp8 || (2 * q > 256 && q < 256)) p.tail_num = tail_num(p);
+    else if (q >= 256) p.splits = 1;
+  } else {
+    p.splits = splits;
+  }
+  if (balanced) {
+    p.units = int64_t(p.B) * p.H * p.units_bh;
+    p.bal_wgs = kBalancedWGs;
+    return RC_OK;
+  }
+  return check_grid(p);
+}
+
 // The per-step attention over either cache format (bf16, or FP8: K8 and V8
 // with their scales).
 rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q_live,
@@ -273,31 +300,11 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
       }
     }
   }
-  // the automatic choice is the one rc_step_auto_splits reports (for either
-  // cache format)
-  if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
-  const bool balanced = splits == kSplitsBalanced;
   Params p;
   memset(&p, 0, sizeof p);
   fill_common(p, B, H, scale);
-  p.bm = rows_per_wg(fp8 ? kQBFp8 : balanced ? kQBBalanced : kQBPlain);
-  RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
-  if (splits == kSplitsTail) {
-    // the FP8 step tiles its queries by 256 rows: keep the tail split only
-    // where those tiles too fill more than half the CUs but not all
-    const int64_t q = int64_t(B) * H * p.n_qtiles;
-    p.splits = 2;
-    if (!fp8 || (2 * q > 256 && q < 256)) p.tail_num = tail_num(p);
-    else if (q >= 256) p.splits = 1;
-  } else {
-    p.splits = splits;
-  }
-  if (balanced) {
-    p.units = int64_t(B) * H * p.units_bh;
-    p.bal_wgs = kBalancedWGs;
-  } else {
-    RC_TRY(check_grid(p));
-  }
+  RC_TRY(plan_step(L, D, fp8, splits, p));
+  const bool balanced = p.splits == kSplitsBalanced;
   p.q = static_cast<const uint16_t*>(q_live);
   p.q_st = tok_stride;
   p.q_sb = tok_stride * n_live;
@@ -391,6 +398,34 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
   p.bm = rows_per_wg(kQBPlain);
   if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
   return auto_splits(p);
+}
+
+rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits, int32_t fp8,
+                               int64_t* work_groups, int32_t* rows_per_wg, int32_t* splits_used) {
+  using namespace rc;
+  RC_TRY(check_layout(L, RC_ENTRY_STEP));
+  if (!work_groups || !rows_per_wg || !splits_used) {
+    set_error("rc_step_launch_shape: null output pointer");
+    return RC_ERR_ARG;
+  }
+  RC_TRY(check_dims(B, H, D, 1.0f));
+  if (splits < kSplitsTail || splits > kMaxSplits || (fp8 != 0 && fp8 != 1)) {
+    set_error("rc_step_launch_shape: splits = %d or fp8 = %d out of range", splits, fp8);
+    return RC_ERR_ARG;
+  }
+  if (fp8 && splits == kSplitsBalanced) {
+    set_error("the balanced schedule is not available with the FP8 cache");
+    return RC_ERR_UNSUPPORTED;
+  }
+  Params p;
+  memset(&p, 0, sizeof p);
+  p.B = B;
+  p.H = H;
+  RC_TRY(plan_step(L, D, fp8 != 0, splits, p));
+  *rows_per_wg = p.bm;
+  *splits_used = p.splits;
+  *work_groups = p.splits == kSplitsBalanced ? int64_t(p.bal_wgs) : int64_t(B) * H * p.n_qtiles * p.splits;
+  return RC_OK;
 }
 
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {

@@ -235,6 +235,35 @@ def test_auto_splits_and_workspace():
     assert L2.auto_splits(1, 1, 128) == 1
 
 
+def test_step_launch_shape():
+    # the headline step: 9 query tiles of 512 rows per head (LT 512 + X 4096)
+    L = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
+    assert L.launch_shape(1, 24, 128) == (216, 512, 1)
+    assert L.launch_shape(1, 24, 128, rc.SPLITS_TAIL) == (432, 512, 2)
+    assert L.launch_shape(1, 24, 128, rc.SPLITS_BALANCED) == (256, 256, rc.SPLITS_BALANCED)
+    assert L.launch_shape(1, 24, 128, 3) == (648, 512, 3)
+    assert L.launch_shape(2, 24, 128, 1) == (432, 512, 1)
+    # the FP8 step tiles by 256 rows (LT 2 + X 16 tiles): 432 tiles fill every CU, no tail
+    assert L.launch_shape(1, 24, 128, 0, fp8=True) == (432, 256, 1)
+    assert L.launch_shape(1, 24, 128, rc.SPLITS_TAIL, fp8=True) == (432, 256, 1)
+    # 15 heads: 135 bf16 tiles take the tail split; 270 FP8 tiles fill the CUs
+    assert L.launch_shape(1, 15, 128) == (270, 512, 2)
+    assert L.launch_shape(1, 15, 128, 0, fp8=True) == (270, 256, 1)
+    # 7 heads: 63 FP8 tiles under the bf16 auto choice of 4 even splits
+    assert L.launch_shape(1, 7, 128, 0, fp8=True) == (4 * 7 * 18, 256, 4)
+    for kw, status in ((dict(D=96), rc.RC_ERR_UNSUPPORTED), (dict(splits=-3), rc.RC_ERR_ARG),
+                       (dict(splits=33), rc.RC_ERR_ARG), (dict(B=0), rc.RC_ERR_ARG),
+                       (dict(splits=rc.SPLITS_BALANCED, fp8=True), rc.RC_ERR_UNSUPPORTED)):
+        args = dict(B=1, H=2, D=128, splits=0, fp8=False)
+        args.update(kw)
+        with pytest.raises(rc.RcError) as e:
+            L.launch_shape(args["B"], args["H"], args["D"], args["splits"], args["fp8"])
+        assert e.value.status == status
+    wg, bm, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+    assert rc.lib().rc_step_launch_shape(ctypes.byref(L.c), 1, 2, 128, 0, 0, None, ctypes.byref(bm),
+                                         ctypes.byref(sp)) == rc.RC_ERR_ARG
+
+
 def test_binding_checks_row_counts():
     """Every read and write is sized from the layout's row count, so the
     binding refuses Q with another token count before anything else (no GPU
