@@ -424,12 +424,13 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
 }
 
 // Optimistic online softmax of one 32-key sub-tile for both query blocks of
-// a wave, used by the ping-pong ring.  While the other wave's MFMAs run, a
-// wave issues a VALU instruction every ~8 cycles and a v_exp_f32 every ~10,
-// so this phase must be short and free of long dependent chains.  The common
-// case does no max reduction: the arguments a = s c - m_used for both blocks
-// (in place), then p = 2^a packed to bf16 P^T, and the row sum over the packed
-// weights (the values the P V product uses) with v_dot2_f32_bf16 in four
+// a wave, used by the ping-pong ring.  Its VALU work issues while the other
+// wave of the SIMD runs its MFMAs, provided it holds no instruction that
+// waits for the matrix unit: v_dot2_f32_bf16 is one (it does not issue while
+// an MFMA is in flight, so a stream of the other wave's MFMAs stalls it), so
+// the row sums use plain fp32 adds.  The common case does no max reduction:
+// the arguments a = s c - m_used for both blocks (in place), then p = 2^a
+// packed to bf16 P^T, and the row sum of the fp32 weights in four
 // independent chains.  If some lane's partial sum leaves [0, 2^16] or is not a
 // number, the running max moves up by max(0, max a) and the weights are
 // recomputed from the shifted arguments (exact up to one fp32 rounding of the
@@ -438,20 +439,21 @@ __device__ __forceinline__ void softmax_part(int lane, int valid, f32x16 (&sacc)
 // the exact path up front: tile max, then the weights.
 constexpr float kSumLimit = 65536.f;
 
-// p = 2^a for one block into P^T (bf16); returns the per-lane sum of the
-// rounded p.
+// p = 2^a for one block into P^T (bf16); returns the per-lane fp32 sum of p
+// in four independent chains of plain adds.  (v_dot2_f32_bf16 would sum the
+// rounded values in half the instructions, but it does not issue while an
+// MFMA of the SIMD is in flight.)
 __device__ __forceinline__ float pack_sum(const f32x16& arg, bf16x8 (&pf)[2]) {
+  float e[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) pf[r >> 3][r & 7] = (__bf16)__builtin_amdgcn_exp2f(arg[r]);
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
-  float a0 = 0.f, a1 = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    a0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[0][2 * i], pf[0][2 * i + 1]}, one, a0, false);
-    a1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[1][2 * i], pf[1][2 * i + 1]}, one, a1, false);
+  for (int r = 0; r < 16; ++r) {
+    e[r] = __builtin_amdgcn_exp2f(arg[r]);
+    pf[r >> 3][r & 7] = (__bf16)e[r];
   }
-  return a0 + a1;
+  float a[4] = {e[0], e[1], e[2], e[3]};
+#pragma unroll
+  for (int r = 4; r < 16; ++r) a[r & 3] += e[r];
+  return (a[0] + a[1]) + (a[2] + a[3]);
 }
 
 template <int D>
