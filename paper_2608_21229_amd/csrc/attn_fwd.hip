@@ -253,7 +253,7 @@ template <int QB>
 struct Blk {
   static constexpr int kSub = QB == 1 ? kBN : 32;  // keys per sub-tile
   static constexpr int kKB = kSub / 32;            // 32-key blocks per sub-tile
-  static constexpr int kPF = QB == 1 ? 3 : 2;      // fragment reads in flight ahead of their MFMAs
+  static constexpr int kPF = 3;                    // fragment reads in flight ahead of their MFMAs
   static constexpr int kRows = 32 * QB * kWaves;   // query rows per work-group
 };
 
