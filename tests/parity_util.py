@@ -13,12 +13,10 @@ from synthgen import ANCHOR, REF, TEXT, TARGET, Workload, bf16_normal, derive_se
 
 MAX_ABS = 2e-2
 REL_L2 = 5e-3
-# LSE: fp32 logits from exact bf16 products and one log of the row sum.  The
-# two-block kernels sum the bf16-rounded weights (the values P.V uses), each
-# within a relative 2^-9 of the exact weight, so ln(sum) is off by at most
-# -ln(1 - 2^-9) = 1.96e-3 (a row whose weight sits on one key); with many keys
-# the round-to-nearest errors cancel (measured ~1e-5).
-LSE_ABS = 2e-3
+# LSE: fp32 logits from exact bf16 products (relative error ~D 2^-24) and one
+# log of an fp32 row sum of the unrounded weights, so the expected error is
+# ~1e-5; 1e-3 leaves two orders of margin.
+LSE_ABS = 1e-3
 
 
 def is_static(kind):
