@@ -1475,12 +1475,13 @@ int launch_attention(const Params& p, int D, void* stream) {
     if (D == 128) q.fp8 ? launch_grid<128, true>(q, nb, s) : launch_grid<128, false>(q, nb, s);
     else q.fp8 ? launch_grid<64, true>(q, nb, s) : launch_grid<64, false>(q, nb, s);
   };
-  // When one batch entry alone fills every CU (at least 256 work-groups), the
-  // entries run as consecutive launches: the last partial round of one
-  // combined grid costs more than the partial rounds of the separate ones
-  // (two guidance branches at 5 references: step 2.70 vs 2.88 ms).  Split-KV
-  // partials are laid out per batch entry, so only unsplit grids do this.
-  if (p.B > 1 && p.splits == 1 && per_batch >= 256) {
+  // When one batch entry alone fills more than half the CUs, the entries run
+  // as consecutive launches: the partial last round of one combined grid
+  // costs more than the idle CUs of the separate ones (five references,
+  // 216 work-groups per entry: B = 2 2.33 vs 2.35-2.59 ms, B = 3 3.53 vs
+  // 3.67 ms).  Split-KV partials are laid out per batch entry, so only
+  // unsplit grids do this.
+  if (p.B > 1 && p.splits == 1 && 2 * per_batch > 256) {
     Params q = p;
     q.B = 1;
     for (int b = 0; b < p.B; ++b) {
