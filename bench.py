@@ -175,6 +175,7 @@ def extras(torch, rc, wl, gen, dev, static, live, step_ms_main):
     q_s, k_s, v_s = static
     q_l, k_l, v_l = live
     anchors = {}
+    runs = {}
     for mask in ("paper", "isolated"):
         Lm = rc.Layout(list(wl.segments), mask)
         ncm = Lm.rows(rc.ROWS_CACHED)
@@ -182,16 +183,25 @@ def extras(torch, rc, wl, gen, dev, static, live, step_ms_main):
         vc = torch.empty_like(kc)
         o_s = torch.empty_like(q_s)
         o_l = torch.empty_like(q_l)
-        pre = time_calls(torch, lambda: rc.ref_kv_prefill(Lm, q_s, k_s, v_s, o=o_s, k_cache=kc, v_cache=vc,
-                                                          scale=wl.scale))
         sp = Lm.auto_splits(B, H, D)
         wsb = Lm.workspace_bytes(B, H, D, sp)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-        stp = time_calls(torch, lambda: rc.step_masked_attention(Lm, q_l, k_l, v_l, kc, vc, o=o_l, splits=sp,
-                                                                 workspace=ws if wsb else None, scale=wl.scale))
-        anchors[mask] = {"prefill_ms": pre, "step_ms": stp, "prefill_pairs": Lm.pairs(rc.ENTRY_PREFILL),
-                         "step_pairs": Lm.pairs(rc.ENTRY_STEP)}
-        del kc, vc, o_s, o_l, ws
+        pre = (lambda Lm=Lm, o_s=o_s, kc=kc, vc=vc:
+               rc.ref_kv_prefill(Lm, q_s, k_s, v_s, o=o_s, k_cache=kc, v_cache=vc, scale=wl.scale))
+        stp = (lambda Lm=Lm, kc=kc, vc=vc, o_l=o_l, sp=sp, ws=ws, wsb=wsb:
+               rc.step_masked_attention(Lm, q_l, k_l, v_l, kc, vc, o=o_l, splits=sp,
+                                        workspace=ws if wsb else None, scale=wl.scale))
+        runs[mask] = (pre, stp)
+        anchors[mask] = {"prefill_ms": float("inf"), "step_ms": float("inf"),
+                         "prefill_pairs": Lm.pairs(rc.ENTRY_PREFILL), "step_pairs": Lm.pairs(rc.ENTRY_STEP)}
+    # the two masks alternate over three rounds and each keeps its fastest
+    # round, so that clock drift between them does not read as overhead
+    for _ in range(3):
+        for mask in ("paper", "isolated"):
+            pre, stp = runs[mask]
+            anchors[mask]["prefill_ms"] = min(anchors[mask]["prefill_ms"], time_calls(torch, pre))
+            anchors[mask]["step_ms"] = min(anchors[mask]["step_ms"], time_calls(torch, stp))
+    del runs
     pa, iso = anchors["paper"], anchors["isolated"]
     anchors["anchor_prefill_overhead_measured"] = pa["prefill_ms"] / iso["prefill_ms"] - 1.0
     anchors["anchor_prefill_overhead_pairs"] = pa["prefill_pairs"] / iso["prefill_pairs"] - 1.0
