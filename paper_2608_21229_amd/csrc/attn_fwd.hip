@@ -903,7 +903,10 @@ struct PPState {
 
 // The four phases of tile t (stage S): softmax of sub-tile 2t, MFMA phase
 // (P V of 2t, S^T of 2t + 1), softmax of 2t + 1, MFMA phase (P V of 2t + 1,
-// S^T of sub-tile 0 of tile t + 1 in stage (S + 1) % 3).
+// S^T of sub-tile 0 of tile t + 1 in stage (S + 1) % 3).  A wave raises its issue
+// priority for its MFMA phases, so that the other wave's softmax instructions
+// fill the gaps between its MFMAs rather than delay them (measured 1-2.5%
+// faster than equal priorities or a raised softmax phase).
 template <int S, int D>
 __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int grp, int lw, int lane,
                                         const bf16x8 (&qf)[2][D / 16], f32x16 (&oacc)[2][D / 32],
@@ -914,6 +917,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   const int valid = tile_valid(st.ccur);
   // softmax of sub-tile 2t; group 1 loads tile t + 2
   ring_barrier();
+  __builtin_amdgcn_s_setprio(0);
   if (grp == 1 && t >= 1 && t + 2 < st.n) {
     issue_tile_pp<D>(st.icur, lw, lane, kbuf<SL>(), vbuf<SL>());
     ++st.issued;
@@ -923,6 +927,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   pin_probs(pf, m_used, lsum);
   // P V of sub-tile 2t, S^T of sub-tile 2t + 1; group 1 then waits for tile t + 1
   ring_barrier();
+  __builtin_amdgcn_s_setprio(3);
   {
     const FragBase fb = phase_base<D>(lane);
     pv_part<D, 2>(vbuf<S>(), fb, 0, pf, oacc);
@@ -932,6 +937,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   if (grp == 1 && t + 1 < st.n) wait_tiles_pp<D>(st.issued - (t + 2));
   // softmax of sub-tile 2t + 1
   ring_barrier();
+  __builtin_amdgcn_s_setprio(0);
   softmax_pp<D>(lane, valid - 32, false, sacc, pf, oacc, m_used, lsum, c);
   pin_probs(pf, m_used, lsum);
   // P V of sub-tile 2t + 1, S^T of the next tile's first sub-tile (after the
@@ -939,6 +945,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   // unused; computing it anyway keeps the old scores from living across this
   // phase)
   ring_barrier();
+  __builtin_amdgcn_s_setprio(3);
   {
     const FragBase fb = phase_base<D>(lane);
     pv_part<D, 2>(vbuf<S>(), fb, 1, pf, oacc);
