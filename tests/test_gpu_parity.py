@@ -227,13 +227,16 @@ def test_ref5_full_recompute_and_step_rows():
     check(ob, O, "ref5 full dense base", rows)
 
 
+@pytest.mark.parametrize("preset", ["perref", "paper"])
 @pytest.mark.parametrize("k", SCALING_KS)
-def test_reference_scaling(k):
-    check_request(workload(f"scaling_k{k}"), "perref", every=61)
+def test_reference_scaling(k, preset):
+    """k references of 4096 tokens under both masks (the figure's mask makes
+    the prefill quadratic in k: the largest prefill the library runs)."""
+    check_request(workload(f"scaling_k{k}"), preset, every=61)
 
 
-def test_reference_scaling_paper_mask_k10():
-    """Ten references under the figure's mask."""
+def test_reference_scaling_paper_mask_k10_last_step():
+    """Ten references under the figure's mask, steps 0 and 39."""
     check_request(workload("scaling_k10"), "paper", every=61, steps=(0, 39))
 
 
