@@ -366,7 +366,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        log("bench.py: this build runs on one GPU only; the multi-GPU split (heads across GPUs, no exchange "
+        log("bench.py: the library runs on one GPU only; the multi-GPU split (heads across GPUs, no exchange "
             "inside attention) is a design note, not an implemented path.  Use --gpus 1.")
         sys.exit(2)
 
