@@ -894,6 +894,59 @@ __device__ __forceinline__ void pin_probs(bf16x8 (&pf)[QB][N], float (&m_used)[Q
   }
 }
 
+// The MFMA phase of the ping-pong ring as one stream of fragment reads: the
+// 2 NB V^T fragments of sub-tile jv (O^T += V^T P^T), then the NDC K
+// fragments of sub-tile jk of ks (S^T = K Q^T), each read kPF fragments ahead
+// of its MFMAs, so that the first K reads are in flight during the last P V
+// MFMAs.  The first kPF V^T fragments arrive in a[] (v_prefetch), read at the
+// end of the softmax phase before, so that the phase's first MFMAs do not wait
+// for the LDS.
+template <int D>
+__device__ __forceinline__ void v_prefetch(const uint16_t* vs, const FragBase& fb, int jv, bf16x8 (&a)[4]) {
+  constexpr int NV = D / 16;  // 2 NB
+#pragma unroll
+  for (int f = 0; f < Blk<2>::kPF; ++f) a[f] = v_frag<D>(vs, fb, jv * NV + f);
+}
+
+template <int D>
+__device__ __forceinline__ void mfma_phase(const uint16_t* vs, const uint16_t* ks, const FragBase& fb, int jv, int jk,
+                                           bf16x8 (&a)[4], const bf16x8 (&pf)[2][2], const bf16x8 (&qf)[2][D / 16],
+                                           f32x16 (&oacc)[2][D / 32], f32x16 (&sacc)[2][1]) {
+  constexpr int NB = D / 32, NDC = D / 16, NV = 2 * NB, NF = NV + NDC;
+  constexpr int PF = Blk<2>::kPF;
+  static_assert(PF + 1 == 4 && NV >= PF, "fragment ring of four");
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    if (f < NV) {
+      const int cc = f / NB, nb = f % NB;
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+        oacc[qb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % 4], pf[qb][cc], oacc[qb][nb], 0, 0, 0);
+    } else {
+      const int dc = f - NV;
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+        sacc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % 4], qf[qb][dc], dc == 0 ? f32x16{} : sacc[qb][0],
+                                                              0, 0, 0);
+    }
+    const int g = f + PF;
+    if (g < NV) a[g % 4] = v_frag<D>(vs, fb, jv * NV + g);
+    else if (g < NF) a[g % 4] = k_frag<D>(ks, fb, jk * NDC + g - NV);
+    sched_fence();
+  }
+}
+
+// Barrier that starts an MFMA phase of the ping-pong ring.  The wave's LDS
+// reads still in flight are the phase's first V^T fragments, of the tile
+// being computed, which no load issued after this barrier overwrites (the
+// loads after a barrier refill the stage of the tile before), so unlike
+// ring_barrier it does not wait for them.  The empty asm statement keeps the
+// reads before the barrier.
+__device__ __forceinline__ void mfma_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+}
+
 struct PPState {
   Cursor icur;  // next tile to load (group 1)
   Cursor ccur;  // tile being computed
@@ -926,12 +979,15 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   softmax_pp<D>(lane, valid, t == 0, sacc, pf, oacc, m_used, lsum, c);
   pin_probs(pf, m_used, lsum);
   // P V of sub-tile 2t, S^T of sub-tile 2t + 1; group 1 then waits for tile t + 1
-  ring_barrier();
-  __builtin_amdgcn_s_setprio(3);
   {
+    sched_fence();
     const FragBase fb = phase_base<D>(lane);
-    pv_part<D, 2>(vbuf<S>(), fb, 0, pf, oacc);
-    s_part<D, 2>(kbuf<S>(), fb, 1, qf, sacc);
+    bf16x8 a[4];
+    v_prefetch<D>(vbuf<S>(), fb, 0, a);
+    sched_fence();
+    mfma_barrier();
+    __builtin_amdgcn_s_setprio(3);
+    mfma_phase<D>(vbuf<S>(), kbuf<S>(), fb, 0, 1, a, pf, qf, oacc, sacc);
     pin_scores(sacc);
   }
   if (grp == 1 && t + 1 < st.n) wait_tiles_pp<D>(st.issued - (t + 2));
@@ -944,12 +1000,15 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   // last tile it reads a stage that holds no new tile and the scores go
   // unused; computing it anyway keeps the old scores from living across this
   // phase)
-  ring_barrier();
-  __builtin_amdgcn_s_setprio(3);
   {
+    sched_fence();
     const FragBase fb = phase_base<D>(lane);
-    pv_part<D, 2>(vbuf<S>(), fb, 1, pf, oacc);
-    s_part<D, 2>(kbuf<SN>(), fb, 0, qf, sacc);
+    bf16x8 a[4];
+    v_prefetch<D>(vbuf<S>(), fb, 1, a);
+    sched_fence();
+    mfma_barrier();
+    __builtin_amdgcn_s_setprio(3);
+    mfma_phase<D>(vbuf<S>(), kbuf<SN>(), fb, 1, 0, a, pf, qf, oacc, sacc);
     pin_scores(sacc);
   }
   if (t + 1 < st.n) cursor_next(p, st.ccur);
