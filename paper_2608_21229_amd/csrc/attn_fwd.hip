@@ -835,11 +835,22 @@ __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b,
 // key masked, so that both groups pass the same barriers.
 constexpr int kLoaders = 4;  // waves of group 1
 
+// The lane index computed afresh (v_mbcnt over a full mask) where it is
+// needed: written as inline assembly so that the compiler neither hoists it
+// out of the tile loop nor keeps it live across the phases, where a register
+// is only to be had by spilling (a spilled lane index costs a scratch reload,
+// a full memory latency, in the phase that issues the tile loads).
+__device__ __forceinline__ int fresh_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Issue the loads of one K/V tile from the loader wave lw of group 1: its
 // instruction i fills the 1 KB chunk c = i * 4 + lw of each tensor, lane l
 // the granule position p = 64 c + l (row p / (D/8), swizzled slot).
 template <int D>
-__device__ __forceinline__ void issue_tile_pp(const Cursor& c, int lw, int lane, uint16_t* ks, uint16_t* vs) {
+__device__ __forceinline__ void issue_tile_pp(const Cursor& c, int lw, uint16_t* ks, uint16_t* vs) {
   constexpr int GR = D / 8;
   constexpr int kLoads = kBN * GR / (kLoaders * 64);
   const uint32_t nrec = uint32_t(min(kBN, c.rem)) * uint32_t(c.st);  // at most 2^31 (see issue_tile)
@@ -847,15 +858,13 @@ __device__ __forceinline__ void issue_tile_pp(const Cursor& c, int lw, int lane,
       __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
   const __amdgpu_buffer_rsrc_t rv =
       __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
-  // the per-lane offsets are recomputed at every issue rather than kept live
-  asm volatile("" : "+v"(lane));
+  const uint32_t lane = uint32_t(fresh_lane());
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
     const int chunk = i * kLoaders + lw;
-    const int pos = chunk * 64 + lane;
-    const int row = pos / GR, slot = pos % GR;
-    const uint32_t voff =
-        uint32_t(row) * uint32_t(c.st) + uint32_t(slot ^ ((((row & 3) << 2) | ((row >> 2) & 3)) & (GR - 1))) * 16u;
+    const uint32_t pos = uint32_t(chunk * 64) + lane;
+    const uint32_t row = pos / GR, slot = pos % GR;
+    const uint32_t voff = row * uint32_t(c.st) + (slot ^ ((((row & 3u) << 2) | ((row >> 2) & 3u)) & (GR - 1))) * 16u;
     dma16(lds_addr(ks + chunk * 512), voff, rk);
     dma16(lds_addr(vs + chunk * 512), voff, rv);
   }
@@ -972,7 +981,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   ring_barrier();
   __builtin_amdgcn_s_setprio(0);
   if (grp == 1 && t >= 1 && t + 2 < st.n) {
-    issue_tile_pp<D>(st.icur, lw, lane, kbuf<SL>(), vbuf<SL>());
+    issue_tile_pp<D>(st.icur, lw, kbuf<SL>(), vbuf<SL>());
     ++st.issued;
     if (t + 3 < st.n) cursor_next(p, st.icur);
   }
@@ -1028,15 +1037,15 @@ __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int
   st.icur = st.ccur;
   st.issued = 0;
   if (grp == 1) {
-    issue_tile_pp<D>(st.icur, lw, lane, kbuf<0>(), vbuf<0>());
+    issue_tile_pp<D>(st.icur, lw, kbuf<0>(), vbuf<0>());
     st.issued = 1;
     if (n > 1) {
       cursor_next(p, st.icur);
-      issue_tile_pp<D>(st.icur, lw, lane, kbuf<1>(), vbuf<1>());
+      issue_tile_pp<D>(st.icur, lw, kbuf<1>(), vbuf<1>());
       st.issued = 2;
       if (n > 2) {
         cursor_next(p, st.icur);
-        issue_tile_pp<D>(st.icur, lw, lane, kbuf<2>(), vbuf<2>());
+        issue_tile_pp<D>(st.icur, lw, kbuf<2>(), vbuf<2>());
         st.issued = 3;
         if (n > 3) cursor_next(p, st.icur);
       }
