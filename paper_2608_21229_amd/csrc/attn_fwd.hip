@@ -59,6 +59,8 @@ typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) const char lds_cchar;
+typedef __attribute__((address_space(3))) const bf16x8 lds_cbf16x8;
 
 constexpr float kLazyThreshold = 8.0f;  // log2 units: rescale when a row max grows by > 2^8
 
@@ -311,10 +313,11 @@ __device__ __forceinline__ bf16x8 k_frag(const uint16_t* ks, const FragBase& fb,
   return *reinterpret_cast<const bf16x8*>(p);
 }
 
-// S^T = K Q^T for sub-tile j (kKB 32x32 accumulators per query block).
-template <int D, int QB>
-__device__ __forceinline__ void s_part(const uint16_t* ks, const FragBase& fb, int j,
-                                       const bf16x8 (&qf)[QB][D / 16], f32x16 (&sacc)[QB][Blk<QB>::kKB]) {
+// S^T = K Q^T for sub-tile j (kKB 32x32 accumulators per query block);
+// src.k(f) reads K fragment f of the stage.
+template <int D, int QB, class Src>
+__device__ __forceinline__ void s_part(const Src& src, int j, const bf16x8 (&qf)[QB][D / 16],
+                                       f32x16 (&sacc)[QB][Blk<QB>::kKB]) {
   constexpr int KB = Blk<QB>::kKB;
   constexpr int NDC = D / 16;
   constexpr int NF = KB * NDC;
@@ -327,7 +330,7 @@ __device__ __forceinline__ void s_part(const uint16_t* ks, const FragBase& fb, i
       for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
   bf16x8 a[PF + 1];
 #pragma unroll
-  for (int f = 0; f < PF && f < NF; ++f) a[f] = k_frag<D>(ks, fb, j * NF + f);
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = src.k(j * NF + f);
   sched_fence();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
@@ -335,7 +338,7 @@ __device__ __forceinline__ void s_part(const uint16_t* ks, const FragBase& fb, i
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
       sacc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], qf[qb][dc], sacc[qb][kb], 0, 0, 0);
-    if (f + PF < NF) a[(f + PF) % (PF + 1)] = k_frag<D>(ks, fb, j * NF + f + PF);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = src.k(j * NF + f + PF);
     sched_fence();
   }
 }
@@ -510,16 +513,81 @@ __device__ __forceinline__ bf16x8 v_frag(const uint16_t* vs, const FragBase& fb,
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// O^T += V^T P^T for sub-tile j: 16 keys per MFMA, 32 d-rows per MFMA.
-template <int D, int QB>
-__device__ __forceinline__ void pv_part(const uint16_t* vs, const FragBase& fb, int j,
-                                        const bf16x8 (&pf)[QB][2 * Blk<QB>::kKB], f32x16 (&oacc)[QB][D / 32]) {
+// Fragments of one ring stage from its pointers and the lane's per-phase
+// bases (the two-block kernels).
+template <int D>
+struct PtrFrags {
+  const uint16_t* ks;
+  const uint16_t* vs;
+  FragBase fb;
+  __device__ __forceinline__ bf16x8 k(int f) const { return k_frag<D>(ks, fb, f); }
+  __device__ __forceinline__ bf16x8 v(int f) const { return v_frag<D>(vs, fb, f); }
+};
+
+// Absolute LDS byte addresses of one stage's fragment reads for one lane:
+// K fragment of d chunk dc at k[dc] (+ 32 D 2 bytes per 32-key block), the
+// two V^T reads of d block nb at v0[nb] and v1[nb] (+ 16 D 2 bytes per 16
+// keys).  The one-block rings compute them once per ring and keep them in
+// registers, which they have to spare; every remaining offset (at most
+// 12 KB) then fits the LDS read's 16-bit offset field wherever the stage lies.
+template <int D>
+struct StageAddr {
+  uint32_t k[D / 16];
+  uint32_t v0[D / 32], v1[D / 32];
+};
+
+template <int D>
+__device__ __forceinline__ StageAddr<D> stage_addr(int lane, const uint16_t* ks, const uint16_t* vs) {
+  const FragBase fb = frag_base<D>(lane);
+  StageAddr<D> a;
+#pragma unroll
+  for (int dc = 0; dc < D / 16; ++dc) a.k[dc] = lds_addr(ks) + (fb.k ^ uint32_t(32 * dc));
+#pragma unroll
+  for (int nb = 0; nb < D / 32; ++nb) {
+    a.v0[nb] = lds_addr(vs) + (fb.v0 ^ uint32_t(64 * nb));
+    a.v1[nb] = lds_addr(vs) + (fb.v1 ^ uint32_t(64 * nb));
+  }
+  // opaque to the optimiser, which would otherwise split the stage base back
+  // out and fold it with the fragment offset (past the offset field's range
+  // for stages high in LDS)
+#pragma unroll
+  for (int dc = 0; dc < D / 16; ++dc) asm volatile("" : "+v"(a.k[dc]));
+#pragma unroll
+  for (int nb = 0; nb < D / 32; ++nb) asm volatile("" : "+v"(a.v0[nb]), "+v"(a.v1[nb]));
+  return a;
+}
+
+template <int D>
+struct AddrFrags {
+  const StageAddr<D>& a;
+  __device__ __forceinline__ bf16x8 k(int f) const {
+    constexpr int NDC = D / 16;
+    const int kb = f / NDC, dc = f % NDC;
+    return *reinterpret_cast<lds_cbf16x8*>(reinterpret_cast<lds_cchar*>(uintptr_t(a.k[dc])) + kb * 32 * D * 2);
+  }
+  __device__ __forceinline__ bf16x8 v(int f) const {
+    constexpr int NB = D / 32;
+    const int cc = f / NB, nb = f % NB;
+    const int off = cc * 16 * D * 2;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(reinterpret_cast<lds_cchar*>(uintptr_t(a.v0[nb])) + off));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(reinterpret_cast<lds_cchar*>(uintptr_t(a.v1[nb])) + off));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
+};
+
+// O^T += V^T P^T for sub-tile j: 16 keys per MFMA, 32 d-rows per MFMA;
+// src.v(f) reads V^T fragment f of the stage.
+template <int D, int QB, class Src>
+__device__ __forceinline__ void pv_part(const Src& src, int j, const bf16x8 (&pf)[QB][2 * Blk<QB>::kKB],
+                                        f32x16 (&oacc)[QB][D / 32]) {
   constexpr int NB = D / 32;
   constexpr int NF = 2 * Blk<QB>::kKB * NB;
   constexpr int PF = Blk<QB>::kPF;
   bf16x8 a[PF + 1];
 #pragma unroll
-  for (int f = 0; f < PF && f < NF; ++f) a[f] = v_frag<D>(vs, fb, j * NF + f);
+  for (int f = 0; f < PF && f < NF; ++f) a[f] = src.v(j * NF + f);
   sched_fence();
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
@@ -527,7 +595,7 @@ __device__ __forceinline__ void pv_part(const uint16_t* vs, const FragBase& fb, 
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
       oacc[qb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[f % (PF + 1)], pf[qb][cc], oacc[qb][nb], 0, 0, 0);
-    if (f + PF < NF) a[(f + PF) % (PF + 1)] = v_frag<D>(vs, fb, j * NF + f + PF);
+    if (f + PF < NF) a[(f + PF) % (PF + 1)] = src.v(j * NF + f + PF);
     sched_fence();
   }
 }
@@ -536,19 +604,19 @@ __device__ __forceinline__ void pv_part(const uint16_t* vs, const FragBase& fb, 
 // S^T = K Q^T, online softmax, O^T += V^T P^T.  A sub-tile wholly past the
 // range end is skipped (valid is wave-uniform).
 template <int D, int QB>
-__device__ __forceinline__ void tile_compute(const uint16_t* ks, const uint16_t* vs, int lane, int valid,
+__device__ __forceinline__ void tile_compute(const StageAddr<D>& sa, int lane, int valid,
                                              const bf16x8 (&qf)[QB][D / 16], f32x16 (&oacc)[QB][D / 32],
                                              float (&m_used)[QB], float (&lsum)[QB], const float (&c)[QB]) {
   constexpr int SUB = Blk<QB>::kSub, KB = Blk<QB>::kKB;
+  const AddrFrags<D> src{sa};
 #pragma unroll
   for (int j = 0; j < kBN / SUB; ++j) {
     if (j > 0 && valid <= j * SUB) break;
-    const FragBase fb = phase_base<D>(lane);
     f32x16 sacc[QB][KB];
     bf16x8 pf[QB][2 * KB];
-    s_part<D, QB>(ks, fb, j, qf, sacc);
+    s_part<D, QB>(src, j, qf, sacc);
     softmax_part<D, QB>(lane, valid - j * SUB, sacc, pf, oacc, m_used, lsum, c);
-    pv_part<D, QB>(vs, fb, j, pf, oacc);
+    pv_part<D, QB>(src, j, pf, oacc);
   }
 }
 
@@ -776,7 +844,8 @@ struct RingState {
 // became free with tile k + kStages - 1, then compute tile k.
 template <int S, int D, int QB>
 __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, int wave, int lane, bool wave_active,
-                                          const uint32_t* voff0, const uint32_t* voff1, RingState& rs,
+                                          const uint32_t* voff0, const uint32_t* voff1, const StageAddr<D>& sa,
+                                          RingState& rs,
                                           const bf16x8 (&qf)[QB][D / 16], f32x16 (&oacc)[QB][D / 32],
                                           float (&m_used)[QB], float (&lsum)[QB], const float (&c)[QB]) {
   constexpr int kLoads = kBN * (D / 8) / kThreads;
@@ -789,7 +858,7 @@ __device__ __forceinline__ void ring_step(const Params& p, int k, int kt_end, in
     if (rs.issued < kt_end) cursor_next(p, rs.icur);
   }
   const int valid = tile_valid(rs.ccur);
-  if (wave_active) tile_compute<D, QB>(kbuf<S>(), vbuf<S>(), lane, valid, qf, oacc, m_used, lsum, c);
+  if (wave_active) tile_compute<D, QB>(sa, lane, valid, qf, oacc, m_used, lsum, c);
   if (k + 1 < kt_end) cursor_next(p, rs.ccur);
 }
 
@@ -803,6 +872,8 @@ __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b,
                                          f32x16 (&oacc)[QB][D / 32], float (&m_used)[QB], float (&lsum)[QB],
                                          const float (&c)[QB]) {
   if (kt_begin >= kt_end) return;
+  const StageAddr<D> sa0 = stage_addr<D>(lane, kbuf<0>(), vbuf<0>());
+  const StageAddr<D> sa1 = stage_addr<D>(lane, kbuf<1>(), vbuf<1>());
   RingState rs;
   rs.icur = cursor_at(p, qs, kt_begin, b, h);
   rs.ccur = rs.icur;
@@ -812,9 +883,10 @@ __device__ __forceinline__ void run_ring(const Params& p, const QSeg& qs, int b,
     if (++rs.issued < kt_end) cursor_next(p, rs.icur);
   }
   for (int kt = kt_begin; kt < kt_end; kt += kStages) {
-    ring_step<0, D, QB>(p, kt, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
+    ring_step<0, D, QB>(p, kt, kt_end, wave, lane, wave_active, voff0, voff1, sa0, rs, qf, oacc, m_used, lsum, c);
     if (kt + 1 >= kt_end) break;
-    ring_step<1, D, QB>(p, kt + 1, kt_end, wave, lane, wave_active, voff0, voff1, rs, qf, oacc, m_used, lsum, c);
+    ring_step<1, D, QB>(p, kt + 1, kt_end, wave, lane, wave_active, voff0, voff1, sa1, rs, qf, oacc, m_used, lsum,
+                        c);
   }
 }
 
@@ -1056,7 +1128,7 @@ __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int
   if (grp == 1) ring_barrier();  // group 1 runs one phase behind group 0
   f32x16 sacc[2][1];
   bf16x8 pf[2][2];
-  s_part<D, 2>(kbuf<0>(), phase_base<D>(lane), 0, qf, sacc);
+  s_part<D, 2>(PtrFrags<D>{kbuf<0>(), vbuf<0>(), phase_base<D>(lane)}, 0, qf, sacc);
   pin_scores(sacc);
   for (int t = 0; t < n; t += 3) {
     pp_tile<0, D>(p, t, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
@@ -1079,7 +1151,7 @@ __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int
 template <int S, int D, int QB>
 __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int tid, int wave, int lane,
                                            bool wave_active, Cursor& icur, Cursor& ccur, float sv,
-                                           const Q8<D> (&q8)[QB], f32x16 (&oacc)[QB][D / 32],
+                                           const StageAddr<D>& sa, const Q8<D> (&q8)[QB], f32x16 (&oacc)[QB][D / 32],
                                            float (&m_used)[QB], float (&lsum)[QB], const float (&cq)[QB]) {
   constexpr int SUB = Blk<QB>::kSub, KB = Blk<QB>::kKB;
   // with two blocks per wave the lane-derived LDS and buffer offsets are
@@ -1106,7 +1178,8 @@ __device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int ti
         if (__any(mt > m_used[qb] + kLazyThreshold)) rescale<D>(oacc[qb], m_used[qb], lsum[qb], mt);
         exp_part(sacc, pf[qb], m_used[qb], lsum[qb], cq[qb]);
       }
-      pv_part<D, QB>(vbuf<S>(), QB == 2 ? phase_base<D>(lane) : frag_base<D>(lane), u, pf, oacc);
+      if constexpr (QB == 1) pv_part<D, QB>(AddrFrags<D>{sa}, u, pf, oacc);
+      else pv_part<D, QB>(PtrFrags<D>{kbuf<S>(), vbuf<S>(), phase_base<D>(lane)}, u, pf, oacc);
     }
   }
   if (j + 1 < n) widen_v8<S ^ 1, D>(tid, sv);
@@ -1131,6 +1204,9 @@ __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b
     const int e = make_q8<D>(qrow[qb], row_ok[qb], lane >> 5, q8[qb]);
     cq[qb] = c * sk * ldexpf(1.f, e);  // scores are s_K 2^e times the accumulated ones
   }
+  // the V^T reads of the widened bf16 stages (the K side reads the 8-bit stages)
+  const StageAddr<D> sa0 = stage_addr<D>(lane, kbuf<0>(), vbuf<0>());
+  const StageAddr<D> sa1 = stage_addr<D>(lane, kbuf<1>(), vbuf<1>());
   Cursor icur = cursor_at(p, qs, kt_begin, b, h);
   Cursor ccur = icur;
   issue_tile8<0, D>(icur, wave, lane, g_k8r[0]);
@@ -1146,9 +1222,10 @@ __device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b
   ring_barrier();
   widen_v8<0, D>(tid, sv);
   for (int j = 0; j < n; j += 2) {
-    ring8_step<0, D, QB>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
+    ring8_step<0, D, QB>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, sa0, q8, oacc, m_used, lsum, cq);
     if (j + 1 >= n) break;
-    ring8_step<1, D, QB>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, q8, oacc, m_used, lsum, cq);
+    ring8_step<1, D, QB>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, sa1, q8, oacc, m_used, lsum,
+                         cq);
   }
 }
 
