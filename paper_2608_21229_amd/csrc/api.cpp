@@ -238,12 +238,8 @@ rc_status plan_step(const rc_layout* L, int32_t D, bool fp8, int32_t splits, Par
   p.bm = rows_per_wg(fp8 ? kQBFp8 : balanced ? kQBBalanced : kQBPlain);
   RC_TRY(plan(L, RC_ENTRY_STEP, p, fp8));
   if (splits == kSplitsTail) {
-    // the FP8 step tiles its queries by 256 rows: keep the tail split only
-    // where those tiles too fill more than half the CUs but not all
-    const int64_t q = int64_t(p.B) * p.H * p.n_qtiles;
     p.splits = 2;
-    if (!fp8 || (2 * q > 256 && q < 256)) p.tail_num = tail_num(p);
-    else if (q >= 256) p.splits = 1;
+    p.tail_num = tail_num(p);
   } else {
     p.splits = splits;
   }

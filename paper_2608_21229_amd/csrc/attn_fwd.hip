@@ -7,8 +7,9 @@
 // of visible key ranges; invisible segments are never loaded.
 //
 // Work-group = 8 waves of 64 lanes, one work-group and two waves per SIMD on
-// each CU.  A wave owns QB blocks of 32 query rows (two in the bf16 kernels:
-// BM = 512; one in the FP8-cache step and the balanced schedule: BM = 256).
+// each CU.  A wave owns QB blocks of 32 query rows (two in the step over
+// either cache, the prefill and the full recompute: BM = 512; one in the
+// balanced schedule: BM = 256).
 // Per 64-key tile:
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = the
 //                   wave's Q rows held in registers for the whole kernel; each
@@ -37,9 +38,9 @@
 // every wave loads and computes whole tiles behind one barrier per tile.
 //
 // Over the FP8 cache (the kF8 instantiation) the fresh key ranges run through
-// the bf16 ring and the cached ranges through a second one: K8 stays 8-bit and
-// S^T = K Q^T runs on the 8-bit MFMA against a two-part e4m3 split of Q, and
-// V8 is widened to bf16 once per tile (see the FP8 cache tiles section).
+// the ping-pong ring and the cached ranges through a second pass of it whose
+// tiles arrive as 8-bit codes and are widened to bf16 in LDS, exactly (the
+// scales are powers of two), one tile ahead of their compute.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -621,67 +622,16 @@ __device__ __forceinline__ void tile_compute(const StageAddr<D>& sa, int lane, i
 }
 
 // ---------------------------------------------------------------- FP8 cache tiles
-// A cached key tile of the FP8 cache (64 key rows of D e4m3fn codes each for
-// K8 and V8) is loaded two tiles ahead of its compute.  K8 stays 8-bit in
-// LDS: S^T = K Q^T runs on the 8-bit MFMA (v_mfma_scale_f32_32x32x64_f8f6f4)
-// against the query rows split into two e4m3 parts (below).  V8 is widened to
-// bf16 one tile ahead by the whole work-group (at D = 128 each lane one
-// 16-byte granule: 8 conversions) into the bf16 ring stage, so P V is the bf16
-// path's.  The scales are powers of two, so widening is exact and the K scale
-// folds into the softmax constant: a cached tile contributes attention over
-// the dequantised cache.
+// Staging slots for the codes of a cache tile of the FP8 cache (64 key rows of
+// D e4m3fn codes each for K8 and V8), which the ping-pong ring widens into
+// its bf16 stages (see the ring below).
 constexpr int kTile8Bytes = kBN * 128;  // bytes per K8 or V8 staging tile (D <= 128)
-// K8: three stages (tile j's codes are read by its QK^T while tile j + 2 loads)
-__shared__ __attribute__((aligned(1024))) char g_k8r[3][kTile8Bytes];
+__shared__ __attribute__((aligned(1024))) char g_k8r[2][kTile8Bytes];
 __shared__ __attribute__((aligned(1024))) char g_v8_0[kTile8Bytes];
 __shared__ __attribute__((aligned(1024))) char g_v8_1[kTile8Bytes];
 
-template <int S>
-__device__ __forceinline__ char* v8buf() {
-  if constexpr (S == 0) return g_v8_0;
-  else return g_v8_1;
-}
-
 __device__ __forceinline__ uint32_t lds_addr8(const char* ptr) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void*)ptr));
-}
-
-// K8 rows in LDS: 16-byte granule g of row r at slot g ^ ((r / (256/D)) &
-// (D/16 - 1)), so the two-granule fragment reads of 32 consecutive rows at
-// one granule pair spread over all bank groups.
-template <int D>
-__device__ __forceinline__ int swz8(int row, int g) {
-  return g ^ ((row / (256 / D)) & (D / 16 - 1));
-}
-
-// DMA of one FP8 tile: the 1 KB chunks w, w + kWaves, ... (of D/16 per
-// tensor) go to wave w; chunk ch of K8 lands in the K8 stage `ks8`
-// (swizzled), of V8 in V8 stage SV at byte 16 p (unswizzled), lane l taking
-// the 16-byte granule p = 64 ch + l (row p / (D/16), granule p % (D/16);
-// cache rows are D bytes apart).  Rows past the range end lie beyond the
-// record count and arrive as zeros.
-template <int D>
-constexpr int kChunks8 = kBN * (D / 16) / 64;
-// loads of one FP8 tile per loading wave (K8 and V8 of each chunk)
-template <int D>
-constexpr int kLoads8 = 2 * ((kChunks8<D> + kWaves - 1) / kWaves);
-
-template <int SV, int D>
-__device__ __forceinline__ void issue_tile8(const Cursor& c, int wave, int lane, char* ks8) {
-  constexpr int GR8 = D / 16;
-  if (wave >= kChunks8<D>) return;
-  const int nrec = min(kBN, c.rem) * D;
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, nrec, 0x00020000);
-#pragma unroll
-  for (int i = 0; i < (kChunks8<D> + kWaves - 1) / kWaves; ++i) {
-    const int ch = wave + i * kWaves;
-    if (ch < kChunks8<D>) {
-      const int pos = ch * 64 + lane, row = pos / GR8, slot = pos % GR8;
-      dma16(lds_addr8(ks8 + ch * 1024), uint32_t(row * D + swz8<D>(row, slot) * 16), rk);
-      dma16(lds_addr8(v8buf<SV>() + ch * 1024), uint32_t(pos * 16), rv);
-    }
-  }
 }
 
 // 16 codes (one 8-bit granule: d = 16 g .. 16 g + 15 of key row `row`) times
@@ -699,120 +649,6 @@ __device__ __forceinline__ void widen_granule(const char* src8, uint16_t* dst, i
   const int row = p / GR8, g = p % GR8;
   *reinterpret_cast<u32x4*>(dst + row * D + swz(row, 2 * g, GR) * 8) = u32x4{e[0], e[1], e[2], e[3]};
   *reinterpret_cast<u32x4*>(dst + row * D + swz(row, 2 * g + 1, GR) * 8) = u32x4{e[4], e[5], e[6], e[7]};
-}
-
-// Widen V8 stage S into bf16 V stage S: thread i takes granules i,
-// i + kThreads, ... (64 D / 16 granules).
-template <int S, int D>
-__device__ __forceinline__ void widen_v8(int tid, float sv) {
-  constexpr int NG = kBN * (D / 16);
-#pragma unroll
-  for (int g = 0; g < (NG + kThreads - 1) / kThreads; ++g) {
-    const int i = tid + g * kThreads;
-    if (NG % kThreads == 0 || i < NG) widen_granule<D>(v8buf<S>(), vbuf<S>(), i, sv);
-  }
-}
-
-// This lane's query row in e4m3 for the 8-bit QK^T: chunk c holds
-// d = 64 c + 32 hh .. +31 (hh = lane / 32; the K8 fragment of the same lane
-// holds the same d).  The row is scaled by 2^-e, e the smallest integer with
-// amax 2^-e <= 448, and split as hi + lo / 16 with both parts e4m3 (round to
-// nearest even): a bf16 value has 8 significant bits, hi keeps 4 and the
-// remainder has at most 4, so the split is exact except for elements below
-// about 2^-11 of the row's largest, whose lowest bits may go (an error below
-// 2^-20 of the row's largest).
-template <int D>
-struct Q8 {
-  i32x8 hi[D / 64], lo[D / 64];
-};
-
-__device__ __forceinline__ int e4m3_exponent(float amax) {
-  if (!(amax > 0.f)) return 0;
-  int k;
-  const float m = frexpf(amax, &k);  // amax = m 2^k, 0.5 <= m < 1; 448 = 0.875 * 2^9
-  return m <= 0.875f ? k - 9 : k - 8;
-}
-
-template <int D>
-__device__ __forceinline__ int make_q8(const uint16_t* qrow, bool row_ok, int hh, Q8<D>& q8) {
-  constexpr int NC = D / 64;
-  // the row stays packed (two bf16 per register) and is unpacked per use
-  u32x4 raw[NC][4];
-#pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-      raw[c][g] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * c + 32 * hh + 8 * g) : u32x4{0u, 0u, 0u, 0u};
-  const auto lo_half = [](uint32_t w) { return __uint_as_float(w << 16); };
-  const auto hi_half = [](uint32_t w) { return __uint_as_float(w & 0xffff0000u); };
-  // amax over the magnitude bits: for finite bf16 values the unsigned order of
-  // (bits & 0x7fff) is the order of |x|, so a packed 16-bit integer max finds it
-  u16x2 mx = {0, 0};
-#pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, raw[c][g][w] & 0x7fff7fffu));
-  float amax = __uint_as_float(uint32_t(mx[0] > mx[1] ? mx[0] : mx[1]) << 16);
-  amax = max_halves(amax);
-  const int e = e4m3_exponent(amax);
-  const float sc = ldexpf(1.f, -e);
-#pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      // elements 4 w .. 4 w + 3 of the 32 this lane holds in chunk c
-      const uint32_t w0 = raw[c][w >> 1][2 * (w & 1)], w1 = raw[c][w >> 1][2 * (w & 1) + 1];
-      const float t0 = lo_half(w0) * sc, t1 = hi_half(w0) * sc;
-      const float t2 = lo_half(w1) * sc, t3 = hi_half(w1) * sc;
-      int hi = __builtin_amdgcn_cvt_pk_fp8_f32(t0, t1, 0, false);
-      hi = __builtin_amdgcn_cvt_pk_fp8_f32(t2, t3, hi, true);
-      const auto b01 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false);
-      const auto b23 = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
-      int lo = __builtin_amdgcn_cvt_pk_fp8_f32((t0 - b01[0]) * 16.f, (t1 - b01[1]) * 16.f, 0, false);
-      lo = __builtin_amdgcn_cvt_pk_fp8_f32((t2 - b23[0]) * 16.f, (t3 - b23[1]) * 16.f, lo, true);
-      q8.hi[c][w] = hi;
-      q8.lo[c][w] = lo;
-    }
-  return e;
-}
-
-// K8 fragment of key block kb, chunk c: row kb*32 + lane%32, bytes
-// d = 64 c + 32 hh .. +31 (two swizzled granules).
-template <int D>
-__device__ __forceinline__ i32x8 k8_frag(const char* ks8, int lane, int kb, int c) {
-  const int row = kb * 32 + (lane & 31);
-  const int g = 4 * c + 2 * (lane >> 5);
-  const u32x4 a = *reinterpret_cast<const u32x4*>(ks8 + row * D + swz8<D>(row, g) * 16);
-  const u32x4 b = *reinterpret_cast<const u32x4*>(ks8 + row * D + swz8<D>(row, g + 1) * 16);
-  return i32x8{int(a[0]), int(a[1]), int(a[2]), int(a[3]), int(b[0]), int(b[1]), int(b[2]), int(b[3])};
-}
-
-// S^T (in units of s_K 2^e) of sub-tile j of an FP8 tile for one query
-// block: per 32-key block and 64-wide chunk of d, one 8-bit MFMA against hi
-// (scale 1) and one against lo (scale 2^-4), accumulating into the same
-// registers.
-template <int D, int KB>
-__device__ __forceinline__ void s_part8(const char* ks8, int lane, int j, const Q8<D>& q8, f32x16 (&sacc)[KB]) {
-  constexpr int NC = D / 64;
-  constexpr int NF = KB * NC;
-#pragma unroll
-  for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-  i32x8 a[2];
-  a[0] = k8_frag<D>(ks8, lane, j * KB, 0);
-  sched_fence();
-#pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    const int kb = f / NC, c = f % NC;
-    if (f + 1 < NF) a[(f + 1) & 1] = k8_frag<D>(ks8, lane, j * KB + (f + 1) / NC, (f + 1) % NC);
-    sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.hi[c], sacc[kb], 0, 0, 0, 127, 0, 127);
-    sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[f & 1], q8.lo[c], sacc[kb], 0, 0, 0, 127, 0, 123);
-    sched_fence();
-  }
 }
 
 // ---------------------------------------------------------------- one-block ring
@@ -1033,15 +869,78 @@ struct PPState {
   Cursor ccur;  // tile being computed
   int issued;   // tiles loaded so far (group 1), counted from the first
   int n;        // tiles of the range
+  float sk, sv; // FP8 cache ring: the (batch, head)'s K and V scales
 };
+
+// ------------------------------------------------ FP8 cache tiles in the ping-pong ring
+// A cache tile (64 rows of D e4m3 codes each for K8 and V8, rows D bytes
+// apart) reaches the ring in two steps, both by group 1: its codes are loaded
+// into one of two staging slots, and one tile later widened (times the
+// power-of-two scales: exact) into the tile's bf16 ring stage, in the layout a
+// fresh tile has, at the end of group 1's first softmax phase of the tile two
+// before it.  From there on it is a bf16 tile.  Tile t + 3 loads into the slot
+// tile t + 1 left, while tile t + 2 is widened out of the other one.
+template <int D>
+constexpr int kChunks8pp = kBN * D / 1024;  // 1 KB chunks of a K8 or V8 tile
+template <int D>
+constexpr int kLoads8pp = 2 * kChunks8pp<D> / kLoaders;  // loads per wave per tile (K8 and V8)
+
+// The FP8 ring's wait: at most n tiles' 8-bit loads of this wave in flight.
+template <int D>
+__device__ __forceinline__ void wait_tiles_pp8(int n) {
+  static_assert(kLoads8pp<D> <= 63, "vmcnt range");
+  if (n <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoads8pp<D>) : "memory");
+}
+
+template <int D>
+__device__ __forceinline__ void issue_tile8_pp(const Cursor& c, int lw, int slot) {
+  static_assert(kChunks8pp<D> % kLoaders == 0, "chunks divide over the loader waves");
+  const uint32_t nrec = uint32_t(min(kBN, c.rem)) * uint32_t(c.st);  // c.st = D bytes: at most 2^13
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.k, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)c.v, (short)0, __builtin_bit_cast(int, nrec), 0x00020000);
+  char* k8 = g_k8r[slot];
+  char* v8 = slot ? g_v8_1 : g_v8_0;
+  const uint32_t lane = uint32_t(fresh_lane());
+#pragma unroll
+  for (int i = 0; i < kChunks8pp<D> / kLoaders; ++i) {
+    const int ch = i * kLoaders + lw;
+    const uint32_t voff = uint32_t(ch * 1024) + lane * 16u;
+    dma16(lds_addr8(k8 + ch * 1024), voff, rk);
+    dma16(lds_addr8(v8 + ch * 1024), voff, rv);
+  }
+}
+
+// Widen staging slot `slot` into bf16 stage S: lane l of loader wave lw takes
+// the 8-bit granules lw * 64 + l + 256 i of K8 and of V8.
+template <int S, int D>
+__device__ __forceinline__ void widen_tile_pp(int lw, int slot, float sk, float sv) {
+  constexpr int NG = kBN * (D / 16);
+  static_assert(NG % (kLoaders * 64) == 0, "granules divide over the loader lanes");
+  const char* k8 = g_k8r[slot];
+  const char* v8 = slot ? g_v8_1 : g_v8_0;
+  const int lane = fresh_lane();
+#pragma unroll
+  for (int i = 0; i < NG / (kLoaders * 64); ++i) {
+    const int pos = i * kLoaders * 64 + lw * 64 + lane;
+    widen_granule<D>(k8, kbuf<S>(), pos, sk);
+    sched_fence();
+    widen_granule<D>(v8, vbuf<S>(), pos, sv);
+    sched_fence();
+  }
+}
 
 // The four phases of tile t (stage S): softmax of sub-tile 2t, MFMA phase
 // (P V of 2t, S^T of 2t + 1), softmax of 2t + 1, MFMA phase (P V of 2t + 1,
 // S^T of sub-tile 0 of tile t + 1 in stage (S + 1) % 3).  A wave raises its issue
 // priority for its MFMA phases, so that the other wave's softmax instructions
 // fill the gaps between its MFMAs rather than delay them (measured 1-2.5%
-// faster than equal priorities or a raised softmax phase).
-template <int S, int D>
+// faster than equal priorities or a raised softmax phase).  In the FP8 ring
+// each phase takes the lane index afresh (fresh_lane): with the widening's
+// registers it would otherwise be spilled and reloaded once per tile.
+template <int S, int D, bool kF8>
 __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int grp, int lw, int lane,
                                         const bf16x8 (&qf)[2][D / 16], f32x16 (&oacc)[2][D / 32],
                                         float (&m_used)[2], float (&lsum)[2], const float (&c)[2],
@@ -1052,17 +951,33 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   // softmax of sub-tile 2t; group 1 loads tile t + 2
   ring_barrier();
   __builtin_amdgcn_s_setprio(0);
-  if (grp == 1 && t >= 1 && t + 2 < st.n) {
+  if constexpr (kF8) {
+    // the codes of tile t + 3 into the slot tile t + 1 left
+    if (grp == 1 && t + 3 < st.n) {
+      issue_tile8_pp<D>(st.icur, lw, (t + 3) & 1);
+      if (t + 4 < st.n) cursor_next(p, st.icur);
+    }
+  } else if (grp == 1 && t >= 1 && t + 2 < st.n) {
     issue_tile_pp<D>(st.icur, lw, kbuf<SL>(), vbuf<SL>());
     ++st.issued;
     if (t + 3 < st.n) cursor_next(p, st.icur);
   }
-  softmax_pp<D>(lane, valid, t == 0, sacc, pf, oacc, m_used, lsum, c);
+  softmax_pp<D>(kF8 ? fresh_lane() : lane, valid, t == 0, sacc, pf, oacc, m_used, lsum, c);
   pin_probs(pf, m_used, lsum);
+  if constexpr (kF8) {
+    // tile t + 2 (its codes landed; tile t + 3's may be in flight) widened into
+    // the stage of tile t - 1, which no wave reads any more
+    if (grp == 1 && t + 2 < st.n) {
+      if (t + 3 < st.n) wait_tiles_pp8<D>(1);
+      else wait_tiles_pp8<D>(0);
+      sched_fence();
+      widen_tile_pp<SL, D>(lw, (t + 2) & 1, st.sk, st.sv);
+    }
+  }
   // P V of sub-tile 2t, S^T of sub-tile 2t + 1; group 1 then waits for tile t + 1
   {
     sched_fence();
-    const FragBase fb = phase_base<D>(lane);
+    const FragBase fb = phase_base<D>(kF8 ? fresh_lane() : lane);
     bf16x8 a[4];
     v_prefetch<D>(vbuf<S>(), fb, 0, a);
     sched_fence();
@@ -1071,11 +986,11 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
     mfma_phase<D>(vbuf<S>(), kbuf<S>(), fb, 0, 1, a, pf, qf, oacc, sacc);
     pin_scores(sacc);
   }
-  if (grp == 1 && t + 1 < st.n) wait_tiles_pp<D>(st.issued - (t + 2));
+  if (!kF8 && grp == 1 && t + 1 < st.n) wait_tiles_pp<D>(st.issued - (t + 2));
   // softmax of sub-tile 2t + 1
   ring_barrier();
   __builtin_amdgcn_s_setprio(0);
-  softmax_pp<D>(lane, valid - 32, false, sacc, pf, oacc, m_used, lsum, c);
+  softmax_pp<D>(kF8 ? fresh_lane() : lane, valid - 32, false, sacc, pf, oacc, m_used, lsum, c);
   pin_probs(pf, m_used, lsum);
   // P V of sub-tile 2t + 1, S^T of the next tile's first sub-tile (after the
   // last tile it reads a stage that holds no new tile and the scores go
@@ -1083,7 +998,7 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   // phase)
   {
     sched_fence();
-    const FragBase fb = phase_base<D>(lane);
+    const FragBase fb = phase_base<D>(kF8 ? fresh_lane() : lane);
     bf16x8 a[4];
     v_prefetch<D>(vbuf<S>(), fb, 1, a);
     sched_fence();
@@ -1095,11 +1010,11 @@ __device__ __forceinline__ void pp_tile(const Params& p, int t, PPState& st, int
   if (t + 1 < st.n) cursor_next(p, st.ccur);
 }
 
-template <int D>
+template <int D, bool kF8 = false>
 __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
                                             int wave, int lane, const bf16x8 (&qf)[2][D / 16],
                                             f32x16 (&oacc)[2][D / 32], float (&m_used)[2], float (&lsum)[2],
-                                            const float (&c)[2]) {
+                                            const float (&c)[2], float sk = 1.f, float sv = 1.f) {
   const int n = kt_end - kt_begin;  // the same for every wave of the work-group
   if (n <= 0) return;
   const int grp = wave >> 2, lw = wave & 3;
@@ -1108,7 +1023,31 @@ __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int
   st.ccur = cursor_at(p, qs, kt_begin, b, h);
   st.icur = st.ccur;
   st.issued = 0;
-  if (grp == 1) {
+  st.sk = sk;
+  st.sv = sv;
+  if (kF8 && grp == 1) {
+    // tiles 0 and 1 loaded and widened into stages 0 and 1; tile 2's codes
+    // then load into slot 0, whose widening reads are done
+    issue_tile8_pp<D>(st.icur, lw, 0);
+    if (n > 1) {
+      cursor_next(p, st.icur);
+      issue_tile8_pp<D>(st.icur, lw, 1);
+      wait_tiles_pp8<D>(1);
+    } else {
+      wait_tiles_pp8<D>(0);
+    }
+    widen_tile_pp<0, D>(lw, 0, sk, sv);
+    if (n > 1) {
+      wait_tiles_pp8<D>(0);
+      widen_tile_pp<1, D>(lw, 1, sk, sv);
+    }
+    if (n > 2) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      cursor_next(p, st.icur);
+      issue_tile8_pp<D>(st.icur, lw, 0);
+      if (n > 3) cursor_next(p, st.icur);
+    }
+  } else if (grp == 1) {
     issue_tile_pp<D>(st.icur, lw, kbuf<0>(), vbuf<0>());
     st.issued = 1;
     if (n > 1) {
@@ -1131,102 +1070,13 @@ __device__ __forceinline__ void run_ring_pp(const Params& p, const QSeg& qs, int
   s_part<D, 2>(PtrFrags<D>{kbuf<0>(), vbuf<0>(), phase_base<D>(lane)}, 0, qf, sacc);
   pin_scores(sacc);
   for (int t = 0; t < n; t += 3) {
-    pp_tile<0, D>(p, t, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+    pp_tile<0, D, kF8>(p, t, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
     if (t + 1 >= n) break;
-    pp_tile<1, D>(p, t + 1, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+    pp_tile<1, D, kF8>(p, t + 1, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
     if (t + 2 >= n) break;
-    pp_tile<2, D>(p, t + 2, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
+    pp_tile<2, D, kF8>(p, t + 2, st, grp, lw, lane, qf, oacc, m_used, lsum, c, sacc, pf);
   }
   if (grp == 0) ring_barrier();  // the barrier group 1 passed at the start
-}
-
-// ---------------------------------------------------------------- FP8 ring
-// Step j of n of the FP8 ring: wait for tile j + 1's loads, barrier (tile
-// j's widened V is visible; bf16 V stage (j + 1) % 2, V8 stage j % 2 and K8
-// stage (j + 2) % 3 are free), load tile j + 2, compute tile j, then widen
-// tile j + 1's V into bf16 stage (j + 1) % 2 (after the compute, so that the
-// tile's MFMAs start right after the barrier).  Blocks take turns on the
-// 8-bit QK^T: a K8 fragment covers 64 d per MFMA, so the K side reads few
-// LDS bytes per MFMA and only the V^T fragments are shared.
-template <int S, int D, int QB>
-__device__ __forceinline__ void ring8_step(const Params& p, int j, int n, int tid, int wave, int lane,
-                                           bool wave_active, Cursor& icur, Cursor& ccur, float sv,
-                                           const StageAddr<D>& sa, const Q8<D> (&q8)[QB], f32x16 (&oacc)[QB][D / 32],
-                                           float (&m_used)[QB], float (&lsum)[QB], const float (&cq)[QB]) {
-  constexpr int SUB = Blk<QB>::kSub, KB = Blk<QB>::kKB;
-  // with two blocks per wave the lane-derived LDS and buffer offsets are
-  // recomputed per tile instead of being kept live across the loop; one
-  // block has the registers to keep them (measured 6% faster so)
-  if constexpr (QB == 2) asm volatile("" : "+v"(lane), "+v"(tid));
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  ring_barrier();
-  if (j + 2 < n) {
-    issue_tile8<S, D>(icur, wave, lane, g_k8r[(j + 2) % 3]);
-    if (j + 3 < n) cursor_next(p, icur);
-  }
-  const int valid = tile_valid(ccur);
-  if (wave_active) {
-#pragma unroll
-    for (int u = 0; u < kBN / SUB; ++u) {
-      if (u > 0 && valid <= u * SUB) break;
-      bf16x8 pf[QB][2 * KB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        f32x16 sacc[KB];
-        s_part8<D, KB>(g_k8r[j % 3], lane, u, q8[qb], sacc);
-        const float mt = tile_max(lane, valid - u * SUB, sacc, cq[qb]);
-        if (__any(mt > m_used[qb] + kLazyThreshold)) rescale<D>(oacc[qb], m_used[qb], lsum[qb], mt);
-        exp_part(sacc, pf[qb], m_used[qb], lsum[qb], cq[qb]);
-      }
-      if constexpr (QB == 1) pv_part<D, QB>(AddrFrags<D>{sa}, u, pf, oacc);
-      else pv_part<D, QB>(PtrFrags<D>{kbuf<S>(), vbuf<S>(), phase_base<D>(lane)}, u, pf, oacc);
-    }
-  }
-  if (j + 1 < n) widen_v8<S ^ 1, D>(tid, sv);
-  if (j + 1 < n) cursor_next(p, ccur);
-}
-
-// The ring over FP8 cache tiles [kt_begin, kt_end): loads run two tiles
-// ahead of the compute, V widening one tile ahead.  qrow: this lane's query
-// row of each block (bf16), read again here to build its e4m3 parts.
-template <int D, int QB>
-__device__ __forceinline__ void run_ring8(const Params& p, const QSeg& qs, int b, int h, int kt_begin, int kt_end,
-                                          int tid, int wave, int lane, bool wave_active,
-                                          const uint16_t* const (&qrow)[QB], const bool (&row_ok)[QB], float sk,
-                                          float sv, f32x16 (&oacc)[QB][D / 32], float (&m_used)[QB],
-                                          float (&lsum)[QB], float c) {
-  const int n = kt_end - kt_begin;
-  if (n <= 0) return;
-  Q8<D> q8[QB];
-  float cq[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int e = make_q8<D>(qrow[qb], row_ok[qb], lane >> 5, q8[qb]);
-    cq[qb] = c * sk * ldexpf(1.f, e);  // scores are s_K 2^e times the accumulated ones
-  }
-  // the V^T reads of the widened bf16 stages (the K side reads the 8-bit stages)
-  const StageAddr<D> sa0 = stage_addr<D>(lane, kbuf<0>(), vbuf<0>());
-  const StageAddr<D> sa1 = stage_addr<D>(lane, kbuf<1>(), vbuf<1>());
-  Cursor icur = cursor_at(p, qs, kt_begin, b, h);
-  Cursor ccur = icur;
-  issue_tile8<0, D>(icur, wave, lane, g_k8r[0]);
-  if (n > 1) {
-    cursor_next(p, icur);
-    issue_tile8<1, D>(icur, wave, lane, g_k8r[1]);
-    if (n > 2) cursor_next(p, icur);
-    // tile 0 landed, tile 1 may be in flight
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoads8<D>) : "memory");
-  } else {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-  ring_barrier();
-  widen_v8<0, D>(tid, sv);
-  for (int j = 0; j < n; j += 2) {
-    ring8_step<0, D, QB>(p, j, n, tid, wave, lane, wave_active, icur, ccur, sv, sa0, q8, oacc, m_used, lsum, cq);
-    if (j + 1 >= n) break;
-    ring8_step<1, D, QB>(p, j + 1, n, tid, wave, lane, wave_active, icur, ccur, sv, sa1, q8, oacc, m_used, lsum,
-                         cq);
-  }
 }
 
 // Logical work-group index: the hardware deals blocks round-robin to the 8
@@ -1253,7 +1103,7 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
   constexpr int kLoads = kBN * GR / kThreads;
   constexpr int BM = Blk<QB>::kRows;
   constexpr int RW = 32 * QB;  // query rows per wave
-  constexpr bool kPingPong = QB == 2 && !kF8;
+  constexpr bool kPingPong = QB == 2;
   static_assert(kLoads >= 1 && kBN * GR % kThreads == 0, "tile granules must divide over the threads");
   static_assert(!kPingPong || kWaves == 2 * kLoaders, "ping-pong pairs waves w and w + 4 on one SIMD");
   const int hh = lane >> 5;  // which 32-lane half
@@ -1302,7 +1152,23 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
     // every wave computes (a wave past the tile's rows holds zero queries and
     // stores nothing): keeping the phases unconditional lets the score and
     // P registers die at each phase instead of living across the next one
-    run_ring_pp<D>(p, qs, b, h, kt_begin, kt_end, wave, lane, qf, oacc, m_used, lsum, cb);
+    if constexpr (kF8) {
+      // the planner puts this segment's fresh (bf16) key ranges before its
+      // FP8 cache ranges: the bf16 ring over the first, the widening ring over
+      // the rest
+      int kt_split = 0;
+      for (int r = qs.r0; r < qs.r0 + qs.nr && p.range[r].src == 0; ++r) kt_split += p.range[r].ntiles;
+      const int mid = min(max(kt_split, kt_begin), kt_end);
+      run_ring_pp<D>(p, qs, b, h, kt_begin, mid, wave, lane, qf, oacc, m_used, lsum, cb);
+      if (mid < kt_end) {
+        if (kt_begin < mid) ring_barrier();  // the first ring's stages are read no more
+        const float sk = p.kv_scale[(int64_t(b) * p.H + h) * 2];
+        const float sv = p.kv_scale[(int64_t(b) * p.H + h) * 2 + 1];
+        run_ring_pp<D, true>(p, qs, b, h, mid, kt_end, wave, lane, qf, oacc, m_used, lsum, cb, sk, sv);
+      }
+    } else {
+      run_ring_pp<D>(p, qs, b, h, kt_begin, kt_end, wave, lane, qf, oacc, m_used, lsum, cb);
+    }
   } else {
     // per-lane byte offsets of this lane's granules inside a tile, per key source
     uint32_t voff0[kLoads], voff1[kLoads];
@@ -1314,30 +1180,8 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
       voff0[i] = uint32_t(row) * uint32_t(p.src[0].k_st) + g16;
       voff1[i] = uint32_t(row) * uint32_t(p.src[1].k_st) + g16;
     }
-    if constexpr (kF8) {
-      // the planner puts this segment's fresh (bf16) key ranges before its FP8
-      // cache ranges: one ring over each kind
-      int kt_split = 0;
-      for (int r = qs.r0; r < qs.r0 + qs.nr && p.range[r].src == 0; ++r) kt_split += p.range[r].ntiles;
-      const int mid = min(max(kt_split, kt_begin), kt_end);
-      run_ring<D, QB>(p, qs, b, h, kt_begin, mid, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum,
-                      cb);
-      if (mid < kt_end) {
-        if (kt_begin < mid) ring_barrier();  // the first ring's stages are read no more
-        // the scales of this (batch, head), read only when cache tiles exist
-        const float sk = p.kv_scale[(int64_t(b) * p.H + h) * 2];
-        const float sv = p.kv_scale[(int64_t(b) * p.H + h) * 2 + 1];
-        const uint16_t* qrow[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          qrow[qb] = p.q + int64_t(b) * p.q_sb + int64_t(row0 + my_row[qb]) * p.q_st + int64_t(h) * D;
-        run_ring8<D, QB>(p, qs, b, h, mid, kt_end, wave * 64 + lane, wave, lane, wave_active, qrow, row_ok, sk, sv,
-                         oacc, m_used, lsum, p.scale_log2);
-      }
-    } else {
-      run_ring<D, QB>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum,
-                      cb);
-    }
+    static_assert(!kF8, "the FP8 cache runs on the ping-pong ring");
+    run_ring<D, QB>(p, qs, b, h, kt_begin, kt_end, wave, lane, wave_active, voff0, voff1, qf, oacc, m_used, lsum, cb);
   }
 
   // ---- epilogue (the half-sum exchange runs on every lane before any lane leaves)

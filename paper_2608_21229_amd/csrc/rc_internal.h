@@ -18,11 +18,12 @@ namespace rc {
 
 constexpr int kWaves = 8;         // waves per work-group (two per SIMD)
 constexpr int kStages = 2;        // K/V tiles resident in LDS in the one-block ring
-// 32-row query blocks per wave.  The bf16 kernels give each wave two blocks
-// (BM = 512 rows per work-group); the FP8-cache step and the balanced
-// schedule keep one (BM = 256), which their registers allow.
+// 32-row query blocks per wave.  The step over either cache, the prefill
+// and the full recompute give each wave two blocks (BM = 512 rows per
+// work-group); the balanced schedule keeps one (BM = 256), which its
+// registers allow.
 constexpr int kQBPlain = 2;
-constexpr int kQBFp8 = 1;
+constexpr int kQBFp8 = 2;
 constexpr int kQBBalanced = 1;
 constexpr int rows_per_wg(int qb) { return 32 * qb * kWaves; }
 constexpr int kBN = 64;           // keys per K/V tile

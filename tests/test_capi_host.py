@@ -243,14 +243,14 @@ def test_step_launch_shape():
     assert L.launch_shape(1, 24, 128, rc.SPLITS_BALANCED) == (256, 256, rc.SPLITS_BALANCED)
     assert L.launch_shape(1, 24, 128, 3) == (648, 512, 3)
     assert L.launch_shape(2, 24, 128, 1) == (432, 512, 1)
-    # the FP8 step tiles by 256 rows (LT 2 + X 16 tiles): 432 tiles fill every CU, no tail
-    assert L.launch_shape(1, 24, 128, 0, fp8=True) == (432, 256, 1)
-    assert L.launch_shape(1, 24, 128, rc.SPLITS_TAIL, fp8=True) == (432, 256, 1)
-    # 15 heads: 135 bf16 tiles take the tail split; 270 FP8 tiles fill the CUs
+    # the FP8 step tiles its queries as the bf16 step does, and splits the same way
+    assert L.launch_shape(1, 24, 128, 0, fp8=True) == (216, 512, 1)
+    assert L.launch_shape(1, 24, 128, rc.SPLITS_TAIL, fp8=True) == (432, 512, 2)
+    # 15 heads: 135 tiles take the tail split
     assert L.launch_shape(1, 15, 128) == (270, 512, 2)
-    assert L.launch_shape(1, 15, 128, 0, fp8=True) == (270, 256, 1)
-    # 7 heads: 63 FP8 tiles under the bf16 auto choice of 4 even splits
-    assert L.launch_shape(1, 7, 128, 0, fp8=True) == (4 * 7 * 18, 256, 4)
+    assert L.launch_shape(1, 15, 128, 0, fp8=True) == (270, 512, 2)
+    # 7 heads: 63 tiles under the automatic choice of 4 even splits
+    assert L.launch_shape(1, 7, 128, 0, fp8=True) == L.launch_shape(1, 7, 128) == (4 * 7 * 9, 512, 4)
     for kw, status in ((dict(D=96), rc.RC_ERR_UNSUPPORTED), (dict(splits=-3), rc.RC_ERR_ARG),
                        (dict(splits=33), rc.RC_ERR_ARG), (dict(B=0), rc.RC_ERR_ARG),
                        (dict(splits=rc.SPLITS_BALANCED, fp8=True), rc.RC_ERR_UNSUPPORTED)):

@@ -70,22 +70,3 @@ def test_quantize_cache_error_and_exactness():
     err = np.abs(deq - c)
     bound = np.maximum(np.abs(c) * 2.0 ** -4, scales[:, :, None, None] * 2.0 ** -10)
     assert (err <= bound * (1 + 1e-12)).all()
-
-
-def test_two_part_e4m3_split_of_bf16_values():
-    """The 8-bit QK^T of the FP8-cache step feeds each query row, scaled by a
-    power of two into e4m3's range, as hi + lo / 16 with hi = e4m3(t) and
-    lo = e4m3(16 (t - hi)).  A bf16 value has 8 significant bits and e4m3
-    keeps 4, so for every bf16 t with 2^-3 <= |t| <= 448 the split is exact;
-    below that (lo in e4m3's subnormal range) the error stays under 2^-13."""
-    bits = np.arange(0, 0x7F80, dtype=np.uint32)           # every finite non-negative bf16 pattern
-    t = (bits << 16).view(np.float32).astype(np.float64)
-    t = t[np.isfinite(t) & (t <= 448.0)]
-    t = np.concatenate([t, -t])
-    hi = of.round_e4m3(t)
-    lo = of.round_e4m3(16.0 * (t - hi))
-    err = np.abs(hi + lo / 16.0 - t)
-    big = np.abs(t) >= 2.0 ** -3
-    assert big.sum() > 2000
-    assert np.all(err[big] == 0.0)
-    assert np.all(err <= 2.0 ** -13)
