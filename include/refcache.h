@@ -177,6 +177,19 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
 rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits, int32_t fp8,
                                int64_t* work_groups, int32_t* rows_per_wg, int32_t* splits_used);
 
+/* Launch plan of rc_ref_kv_prefill (bf16 cache), for reports and tests:
+ * *attn_wgs attention work-groups over all launches (one per query tile),
+ * *copy_wgs copy work-groups appended to the (last) attention launch, and
+ * *copy_rows the flat cache rows (b, h, row) [0, *copy_rows) that they
+ * copy; the store kernel copies the other B * H * N_cached - *copy_rows rows
+ * after the attention.  The copy work-groups run on the CUs that the
+ * attention grid's partial last round leaves free, and take as many rows as
+ * a dispatch model of that round says fit there.  Host only; RC_ERR_ARG on
+ * bad arguments or null outputs, RC_ERR_MASK_NOT_CACHEABLE as the
+ * prefill. */
+rc_status rc_prefill_launch_plan(const rc_layout* L, int32_t B, int32_t H, int32_t D, int64_t* attn_wgs,
+                                 int32_t* copy_wgs, int64_t* copy_rows);
+
 /* Static-subgraph prefill (Sec. 3.3; App. C, Eq. cost-pre).
  *   q_static, k_static, v_static  [B, N_static, H, D]: the ST and R tokens in
  *                                 sequence order (RC_ROWS_STATIC rows).

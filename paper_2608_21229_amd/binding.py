@@ -70,6 +70,8 @@ SIGNATURES = {
                                                 _vp, _i32, _vp]),
     "rc_step_launch_shape": (_i32, [_PL, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64),
                                     ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
+    "rc_prefill_launch_plan": (_i32, [_PL, _i32, _i32, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_i32),
+                                      ctypes.POINTER(_i64)]),
     "rc_status_string": (ctypes.c_char_p, [_i32]),
     "rc_last_error": (ctypes.c_char_p, []),
 }
@@ -150,6 +152,14 @@ class Layout:
         _check(lib().rc_step_launch_shape(ctypes.byref(self.c), B, H, D, splits, int(fp8), ctypes.byref(wg),
                                           ctypes.byref(bm), ctypes.byref(sp)))
         return wg.value, bm.value, sp.value
+
+    def prefill_plan(self, B: int, H: int, D: int):
+        """(attention work-groups, copy work-groups, cache rows they copy) of
+        the bf16 prefill; the store kernel copies the remaining rows."""
+        a, c, r = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+        _check(lib().rc_prefill_launch_plan(ctypes.byref(self.c), B, H, D, ctypes.byref(a), ctypes.byref(c),
+                                            ctypes.byref(r)))
+        return a.value, c.value, r.value
 
     def auto_splits(self, B: int, H: int, D: int) -> int:
         return int(lib().rc_step_auto_splits(ctypes.byref(self.c), B, H, D))

@@ -198,10 +198,32 @@ rc_status prefill_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, floa
       for (int i = 0; i < n_copy; ++i) c.seg[i] = seg[i];
       c.total_rows = int32_t(n_cached);
     }
-    // cache store: one thread per 16-byte granule, 256 per work-group
-    RC_TRY(check_blocks((int64_t(B) * H * n_cached * (D / 8) + 255) / 256, "cache store"));
+    // Copy work-groups at the end of the attention grid take the cache rows
+    // that fit on the CUs its partial last round leaves free; the store
+    // kernel (one thread per 16-byte granule, 256 per work-group) the rest.
+    const CopyPlan cpl = plan_copy_tail(p, n_cached);
+    if (cpl.blocks > 0) {
+      CopyTail& t = p.cp;
+      t.k_src = c.k_src;
+      t.v_src = c.v_src;
+      t.k_dst = c.k_dst;
+      t.v_dst = c.v_dst;
+      t.src_sb = c.src_sb;
+      t.src_st = c.src_st;
+      t.B = B;
+      t.H = H;
+      t.n_cached = c.n_cached;
+      t.n_copy = c.n_copy;
+      for (int i = 0; i < n_copy; ++i) t.seg[i] = seg[i];
+      t.blocks = cpl.blocks;
+      t.rows = int32_t(cpl.rows);
+      RC_TRY(check_blocks(int64_t(B) * H * p.n_qtiles + cpl.blocks, "prefill attention"));
+    }
+    c.row0 = cpl.rows;
+    const int64_t rest = int64_t(B) * H * n_cached - cpl.rows;
+    RC_TRY(check_blocks((rest * (D / 8) + 255) / 256, "cache store"));
     RC_TRY(hip_status(launch_attention(p, D, stream), "prefill attention launch"));
-    if (n_cached > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
+    if (rest > 0) RC_TRY(hip_status(launch_cache_store(c, stream), "cache store launch"));
     return RC_OK;
   }
   CacheStore8Params c;
@@ -394,6 +416,27 @@ int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D)
   p.bm = rows_per_wg(kQBPlain);
   if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 1;
   return auto_splits(p);
+}
+
+rc_status rc_prefill_launch_plan(const rc_layout* L, int32_t B, int32_t H, int32_t D, int64_t* attn_wgs,
+                                 int32_t* copy_wgs, int64_t* copy_rows) {
+  using namespace rc;
+  RC_TRY(check_layout(L, RC_ENTRY_PREFILL));
+  if (!attn_wgs || !copy_wgs || !copy_rows) {
+    set_error("rc_prefill_launch_plan: null output pointer");
+    return RC_ERR_ARG;
+  }
+  RC_TRY(check_dims(B, H, D, 1.0f));
+  Params p;
+  memset(&p, 0, sizeof p);
+  fill_common(p, B, H, 1.0f);
+  p.bm = rows_per_wg(kQBPlain);
+  RC_TRY(plan(L, RC_ENTRY_PREFILL, p));
+  const CopyPlan c = plan_copy_tail(p, count_cached_rows(L));
+  *attn_wgs = int64_t(B) * H * p.n_qtiles;
+  *copy_wgs = c.blocks;
+  *copy_rows = c.rows;
+  return RC_OK;
 }
 
 rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits, int32_t fp8,

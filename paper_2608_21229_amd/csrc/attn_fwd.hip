@@ -1228,24 +1228,78 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
   }
 }
 
-// One work-group per (batch, head, query tile, key split).  The host plans
-// the query tiles with p.bm = rows_per_wg of the kernel's block count.
+// Copy work-group j of the prefill's cache store: rows [j R / C, (j + 1) R /
+// C) of the first R = c.rows flat cache rows ([B, H, n_cached] rows of D
+// values), D / 8 lanes per row, eight rows per lane in flight before their
+// stores.  Work-groups are dispatched in order, so these
+// start when the last attention work-groups have been placed and take the
+// CUs that the partial last round leaves free.  Loads and stores bypass the
+// caches' retention (the attention work-groups still running read their
+// keys through L2).
+template <int D>
+__device__ __forceinline__ void copy_tail(const CopyTail& c, int j, int tid) {
+  constexpr int GR = D / 8, RPP = kThreads / GR, U = 8;
+  const uint32_t H = uint32_t(c.H);
+  const uint32_t R = uint32_t(c.rows);  // <= B H n_cached < 2^31 (host check)
+  const uint32_t r0 = uint32_t(uint64_t(R) * uint32_t(j) / uint32_t(c.blocks));
+  const uint32_t r1 = uint32_t(uint64_t(R) * uint32_t(j + 1) / uint32_t(c.blocks));
+  const int g8 = (tid % GR) * 8;
+  for (uint32_t base = r0 + uint32_t(tid / GR); base < r1; base += uint32_t(RPP * U)) {
+    u32x4 kx[U], vx[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t r = base + uint32_t(u * RPP);
+      if (r < r1) {
+        const uint32_t bh = r / uint32_t(c.n_cached), drow = r - bh * uint32_t(c.n_cached);
+        const uint32_t b = bh / H, h = bh - b * H;
+        int si = 0;
+        while (si + 1 < c.n_copy && uint32_t(c.seg[si + 1].dst_row0) <= drow) ++si;
+        const int64_t srow = int64_t(c.seg[si].src_row0) + int64_t(drow) - c.seg[si].dst_row0;
+        const int64_t so = int64_t(b) * c.src_sb + srow * c.src_st + int64_t(h) * D + g8;
+        kx[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(c.k_src + so));
+        vx[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(c.v_src + so));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t r = base + uint32_t(u * RPP);
+      if (r < r1) {
+        const int64_t dof = int64_t(r) * D + g8;
+        __builtin_nontemporal_store(kx[u], reinterpret_cast<u32x4*>(c.k_dst + dof));
+        __builtin_nontemporal_store(vx[u], reinterpret_cast<u32x4*>(c.v_dst + dof));
+      }
+    }
+  }
+}
+
+// One work-group per (batch, head, query tile, key split), then p.cp.blocks
+// copy work-groups (the prefill's cache store; unsplit bf16 launches only).
+// The host plans the query tiles with p.bm = rows_per_wg of the kernel's
+// block count.
 template <int D, bool kSplit, bool kF8>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   constexpr int QB = kF8 ? kQBFp8 : kQBPlain;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int n_attn = gridDim.x;
+  if constexpr (!kSplit && !kF8) {
+    n_attn -= p.cp.blocks;
+    if (int(blockIdx.x) >= n_attn) {
+      copy_tail<D>(p.cp, blockIdx.x - n_attn, tid);
+      return;
+    }
+  }
   int split, rest;
   if (kSplit && p.tail_num > 0) {
     // tail split: blocks [0, Q) are the long pieces, dispatched first; blocks
     // [Q, 2 Q) the short ones.  Both halves map to query tiles the same way,
     // so (for Q a multiple of 8) a tile's short piece runs on the XCD of its
     // long piece, where the other short pieces of the head share its keys.
-    const int q = gridDim.x / 2;
+    const int q = n_attn / 2;
     split = blockIdx.x >= q;
     rest = xcd_logical_block(blockIdx.x - split * q, q);
   } else {
-    const int w = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int w = xcd_logical_block(blockIdx.x, n_attn);
     split = w % p.splits;
     rest = w / p.splits;
   }
@@ -1408,10 +1462,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams c) {
     c.lse[bhr] = l > 0.f ? M * 0.69314718055994531f + __logf(l) : -INFINITY;
 }
 
-// Cache store: one thread per 16-byte granule of one cached (b, h, row).
+// Cache store: one thread per 16-byte granule of one cached (b, h, row),
+// from flat row c.row0 on.
 __global__ __launch_bounds__(256) void cache_store_kernel(const CacheStoreParams c) {
   const int gr = c.D / 8;
-  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t idx = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) + c.row0 * gr;
   const int64_t total = int64_t(c.B) * c.H * c.total_rows * gr;
   if (idx >= total) return;
   const int g = int(idx % gr);
@@ -1467,8 +1522,12 @@ int launch_attention(const Params& p, int D, void* stream) {
   const int64_t per_batch = int64_t(p.H) * p.n_qtiles * p.splits;
   const int64_t blocks = int64_t(p.B) * per_batch;
   if (blocks == 0) return 0;
+  // copy work-groups ride on unsplit bf16 grids only (the other kernels have
+  // no copy path)
+  if (p.cp.blocks < 0 || (p.cp.blocks > 0 && (p.splits != 1 || p.fp8))) return int(hipErrorInvalidValue);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const auto launch = [&](const Params& q, int64_t nb) {
+    nb += q.cp.blocks;
     if (D == 128) q.fp8 ? launch_grid<128, true>(q, nb, s) : launch_grid<128, false>(q, nb, s);
     else q.fp8 ? launch_grid<64, true>(q, nb, s) : launch_grid<64, false>(q, nb, s);
   };
@@ -1478,10 +1537,11 @@ int launch_attention(const Params& p, int D, void* stream) {
   // 216 work-groups per entry: B = 2 2.33 vs 2.35-2.59 ms, B = 3 3.53 vs
   // 3.67 ms).  Split-KV partials are laid out per batch entry, so only
   // unsplit grids do this.
-  if (p.B > 1 && p.splits == 1 && 2 * per_batch > 256) {
+  if (per_batch_launches(p)) {
     Params q = p;
     q.B = 1;
     for (int b = 0; b < p.B; ++b) {
+      q.cp.blocks = b == p.B - 1 ? p.cp.blocks : 0;  // the copy rides on the last launch
       q.q = p.q + int64_t(b) * p.q_sb;
       q.o = p.o + int64_t(b) * p.o_sb;
       q.lse = p.lse ? p.lse + int64_t(b) * p.H * p.n_rows : nullptr;
@@ -1524,7 +1584,7 @@ int launch_combine(const CombineParams& c, void* stream) {
 }
 
 int launch_cache_store(const CacheStoreParams& c, void* stream) {
-  const int64_t total = int64_t(c.B) * c.H * c.total_rows * (c.D / 8);
+  const int64_t total = (int64_t(c.B) * c.H * c.total_rows - c.row0) * (c.D / 8);
   if (total == 0) return 0;
   hipLaunchKernelGGL(cache_store_kernel, dim3((total + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream), c);
   return int(hipGetLastError());

@@ -10,6 +10,11 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+#include <functional>
+#include <queue>
+#include <vector>
+
 #include "rc_internal.h"
 
 namespace rc {
@@ -247,6 +252,74 @@ int32_t auto_splits(const Params& p) {
   if (s > cap) s = cap;
   if (s > kMaxSplits) s = kMaxSplits;
   return s < 1 ? 1 : int32_t(s);
+}
+
+bool per_batch_launches(const Params& p) {
+  return p.B > 1 && p.splits == 1 && 2 * int64_t(p.H) * p.n_qtiles > kCUs;
+}
+
+// Dispatch model of one unsplit attention launch: work-group i goes to XCD
+// i mod 8 and there, in order, to the first of the XCD's 32 CUs to become
+// free; a work-group lasts its query tile's key tiles plus kTileOverhead
+// tile times.  The copy work-groups come after the last attention
+// work-group, at most one on each CU the partial last round leaves free,
+// and may run until the attention ends: a CU copies about kCopyRowsPerTile cache rows
+// (K and V of one token and head) per tile time (measured: about 100 at
+// D = 128, 512-row tiles).  The model stops at kMaxModelWGs work-groups,
+// where the store is a small part of the launch.
+namespace {
+constexpr int64_t kCopyRowsPerTile = 64;
+constexpr int64_t kTileOverhead = 2;
+constexpr int64_t kCopyMinRows = 64;  // per copy work-group
+constexpr int64_t kMaxModelWGs = int64_t(1) << 16;
+}  // namespace
+
+CopyPlan plan_copy_tail(const Params& p, int64_t n_cached) {
+  const CopyPlan none{0, 0};
+  if (n_cached <= 0 || p.splits != 1 || p.fp8) return none;
+  const int64_t R = int64_t(p.B) * p.H * n_cached;
+  if (R >= (int64_t(1) << 31)) return none;  // the copy work-groups index rows in 32 bits
+  const int64_t A = per_batch_launches(p) ? int64_t(p.H) * p.n_qtiles : int64_t(p.B) * p.H * p.n_qtiles;
+  if (A <= 0 || A > kMaxModelWGs || A % kCUs == 0) return none;
+  const int64_t C = kCUs - A % kCUs;
+  constexpr int kXcds = 8, kPerXcd = kCUs / kXcds;
+  typedef std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> FreeAt;
+  std::vector<FreeAt> cu(kXcds);
+  for (auto& q : cu)
+    for (int i = 0; i < kPerXcd; ++i) q.push(0);
+  // the kernel's block -> (query tile) mapping: consecutive logical blocks
+  // on one XCD
+  const int64_t per = A >> 3, rem = A & 7;
+  int64_t end = 0;
+  for (int64_t bid = 0; bid < A; ++bid) {
+    const int64_t x = bid & 7, kx = bid >> 3;
+    const int64_t w = x < rem ? x * (per + 1) + kx : rem * (per + 1) + (x - rem) * per + kx;
+    const int t = int(w % p.n_qtiles);
+    int qi = 0;
+    while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
+    FreeAt& q = cu[size_t(x)];
+    const int64_t fin = q.top() + p.qseg[qi].ktiles + kTileOverhead;
+    q.pop();
+    q.push(fin);
+    end = std::max(end, fin);
+  }
+  // Copy work-groups take equal row counts, so the one with the shortest
+  // window sets the pace: keep the first c of them (those placed earliest)
+  // with the largest c x (shortest window among them), and no more than
+  // give each kCopyMinRows rows.
+  std::vector<int64_t> win(static_cast<size_t>(C), 0);
+  int64_t window = end, best_c = 0;
+  for (int64_t j = 0; j < C; ++j) {
+    FreeAt& q = cu[size_t((A + j) & 7)];
+    window = std::min(window, end - q.top());
+    q.pop();  // the copy keeps its CU
+    win[size_t(j)] = window;
+    if ((j + 1) * window > (best_c ? best_c * win[size_t(best_c - 1)] : 0)) best_c = j + 1;
+  }
+  const int64_t c = std::min(best_c, R / kCopyMinRows);
+  if (c <= 0) return none;
+  const int64_t rows = std::min(R, c * kCopyRowsPerTile * win[size_t(c - 1)]);
+  return CopyPlan{int32_t(c), rows};
 }
 
 int32_t tail_num(const Params& p) {

@@ -16,6 +16,7 @@
 
 namespace rc {
 
+constexpr int kCUs = 256;         // compute units of the MI355X
 constexpr int kWaves = 8;         // waves per work-group (two per SIMD)
 constexpr int kStages = 2;        // K/V tiles resident in LDS in the one-block ring
 // 32-row query blocks per wave.  The step over either cache, the prefill
@@ -52,6 +53,27 @@ struct QSeg {
   int32_t ktiles;  // key tiles over all its ranges
 };
 
+// A run of cached rows: static-buffer rows [src_row0, src_row0 + len) go to
+// cache rows [dst_row0, dst_row0 + len).
+struct CopySeg {
+  int32_t src_row0, len, dst_row0;
+};
+
+// The bf16 cache store carried by the prefill's attention launch: `blocks`
+// work-groups after the attention work-groups copy the cached rows, on the
+// CUs that the attention grid's partial last round leaves idle.
+struct CopyTail {
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  uint16_t* k_dst;
+  uint16_t* v_dst;
+  int64_t src_sb, src_st;  // element strides of the static K/V: batch, token
+  int32_t B, H, n_cached, n_copy;
+  int32_t blocks;          // copy work-groups at the end of the grid (0: none)
+  int32_t rows;            // flat cache rows (b, h, row) [0, rows) that they copy
+  CopySeg seg[RC_MAX_SEGMENTS];
+};
+
 // A key source, addressed in bytes.  bf16 sources hold K and V as
 // [B, N, H, D] with one token stride; the FP8 cache holds K8 and V8 as
 // [B, H, N_cached, D] bytes.
@@ -82,19 +104,18 @@ struct Params {
   float scale_log2;    // softmax scale * log2(e)
   QSeg qseg[RC_MAX_SEGMENTS];
   KeyRange range[kMaxRanges];
+  CopyTail cp;         // prefill only; cp.blocks = 0 elsewhere
 };
 
 // Cache store: copy rows of the cached segments from the static K/V buffers
 // ([B, N_static, H, D], token stride) into the cache ([B, H, N_cached, D]).
-struct CopySeg {
-  int32_t src_row0, len, dst_row0;
-};
 struct CacheStoreParams {
   const uint16_t* k_src;
   const uint16_t* v_src;
   uint16_t* k_dst;
   uint16_t* v_dst;
   int64_t src_sb, src_st;
+  int64_t row0;        // first flat cache row (b, h, row) this launch copies
   int32_t B, H, D, n_cached, n_copy, total_rows;
   CopySeg seg[RC_MAX_SEGMENTS];
 };
@@ -149,10 +170,21 @@ int64_t count_cached_rows(const rc_layout* L);
 rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first = false);
 int32_t auto_splits(const Params& p);
 int32_t tail_num(const Params& p);  // the long split's share of the key tiles, in 1/1024
+// The prefill's bf16 cache store: the copy work-groups appended to the
+// attention grid and the flat cache rows [0, rows) they take; the store
+// kernel copies the rest.
+struct CopyPlan {
+  int32_t blocks;
+  int64_t rows;
+};
+CopyPlan plan_copy_tail(const Params& p, int64_t n_cached);
 
 void set_error(const char* fmt, ...);
 
 // Kernel launchers (attn_fwd.hip).  Return a hipError_t as int.
+// Unsplit multi-batch grids that run one launch per batch entry (each entry
+// alone fills more than half the CUs).
+bool per_batch_launches(const Params& p);
 int launch_attention(const Params& p, int D, void* stream);
 int launch_combine(const CombineParams& c, void* stream);
 int launch_attention_balanced(const Params& p, int D, void* stream);

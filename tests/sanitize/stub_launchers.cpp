@@ -99,6 +99,16 @@ namespace rc {
 
 int launch_attention(const Params& p, int D, void*) {
   check_params(p, D, false);
+  const CopyTail& c = p.cp;
+  REQUIRE(c.blocks >= 0 && c.blocks < kCUs, c.blocks, 0);
+  if (c.blocks > 0) {
+    REQUIRE(p.splits == 1 && !p.fp8, p.splits, p.fp8);
+    REQUIRE(c.k_src && c.v_src && c.k_dst && c.v_dst, 0, 0);
+    REQUIRE(c.B == p.B && c.H == p.H, c.B, c.H);
+    REQUIRE(int64_t(c.B) * c.H * c.n_cached < (int64_t(1) << 31), c.n_cached, 0);
+    REQUIRE(c.rows >= c.blocks && c.rows <= int64_t(c.B) * c.H * c.n_cached, c.rows, c.blocks);
+    check_copy(c.seg, c.n_copy, c.n_cached);
+  }
   ++g_launches;
   return 0;
 }
@@ -126,6 +136,7 @@ int launch_combine(const CombineParams& c, void*) {
 int launch_cache_store(const CacheStoreParams& c, void*) {
   REQUIRE(c.k_src && c.v_src && c.k_dst && c.v_dst, 0, 0);
   REQUIRE(c.total_rows == c.n_cached, c.total_rows, c.n_cached);
+  REQUIRE(c.row0 >= 0 && c.row0 < int64_t(c.B) * c.H * c.n_cached, c.row0, c.n_cached);
   check_copy(c.seg, c.n_copy, c.n_cached);
   ++g_launches;
   return 0;

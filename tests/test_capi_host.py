@@ -264,6 +264,51 @@ def test_step_launch_shape():
                                          ctypes.byref(sp)) == rc.RC_ERR_ARG
 
 
+def test_prefill_launch_plan():
+    """The bf16 prefill's cache store split: copy work-groups appended to the
+    attention grid (at most one per CU its partial last round leaves free)
+    take the first rows, the store kernel the rest."""
+    head = [(0, 64), (1, 512), (2, 4096)]
+    # five references, per-reference mask: 41 query tiles x 24 heads = 984
+    # work-groups; 40 CUs idle in the last round, where the model fits 35%
+    # of the 24 x 20 544 cache rows
+    L5 = rc.Layout(head + [(3, 4096)] * 5, "perref")
+    assert L5.prefill_plan(1, 24, 128) == (984, 40, 171520)
+    # one reference: a single partial round; every row goes with the attention
+    L1 = rc.Layout(head + [(3, 4096)], "perref")
+    assert L1.prefill_plan(1, 24, 128) == (216, 40, 24 * 4160)
+    # the paper mask's references read each other: long work-groups, the whole cache fits
+    Lp = rc.Layout(head + [(3, 4096)] * 5, "paper")
+    a, c, r = Lp.prefill_plan(1, 24, 128)
+    assert (a, c, r) == (984, 40, 24 * Lp.rows(rc.ROWS_CACHED))
+    # 256 work-groups fill whole rounds: no copy work-groups
+    Ls = rc.Layout([(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "perref")
+    assert Ls.prefill_plan(2, 32, 64) == (256, 0, 0)
+    rng = random.Random(5)
+    for _ in range(300):
+        kinds, lens = random_layout(rng)
+        L = rc.Layout(list(zip(kinds, lens)), "perref")
+        B, H = rng.choice([1, 2, 3]), rng.choice([1, 2, 5, 24, 64])
+        try:
+            a, c, r = L.prefill_plan(B, H, 128)
+        except rc.RcError as e:
+            assert e.status == rc.RC_ERR_MASK_NOT_CACHEABLE
+            continue
+        total = B * H * L.rows(rc.ROWS_CACHED)
+        assert 0 <= c < 256 and 0 <= r <= total
+        assert (c == 0) == (r == 0)
+        if c:
+            assert r >= c * 64 and (a % 256 == 0 or c <= 256 - a % 256 or B > 1)
+    for kw in (dict(D=96), dict(B=0), dict(H=0)):
+        args = dict(B=1, H=2, D=128)
+        args.update(kw)
+        with pytest.raises(rc.RcError):
+            L5.prefill_plan(args["B"], args["H"], args["D"])
+    a, c = ctypes.c_int64(), ctypes.c_int32()
+    assert rc.lib().rc_prefill_launch_plan(ctypes.byref(L5.c), 1, 2, 128, ctypes.byref(a), ctypes.byref(c),
+                                           None) == rc.RC_ERR_ARG
+
+
 def test_binding_checks_row_counts():
     """Every read and write is sized from the layout's row count, so the
     binding refuses Q with another token count before anything else (no GPU

@@ -109,6 +109,43 @@ def test_ragged_segments(name, segs, preset, D):
         check_request(wl, preset, splits=splits)
 
 
+# The prefill's bf16 cache store in each of its three forms: copy work-groups
+# at the end of the attention grid take every cached row ("tail"), the rows
+# that fit while the store kernel copies the rest ("split"), or none
+# ("store": the attention grid fills whole rounds).  Ragged segments, several
+# batch entries, one launch per batch entry (B = 2, H = 64), the paper mask.
+RAGGED5 = [(0, 50), (1, 64), (2, 256), (3, 300), (3, 77)]
+CACHE_STORE = [
+    ("tail_only", RAGGED5, "perref", 1, 8, 128, "tail"),
+    ("split_ragged", RAGGED5, "perref", 3, 29, 128, "split"),
+    ("split_per_batch", RAGGED5, "perref", 2, 64, 64, "split"),
+    ("split_paper", RAGGED5, "paper", 1, 72, 64, "split"),
+    ("store_only", [(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "perref", 2, 32, 64, "store"),
+]
+
+
+@pytest.mark.parametrize("name,segs,preset,B,H,D,regime", CACHE_STORE)
+def test_prefill_cache_store_forms(name, segs, preset, B, H, D, regime):
+    from synthgen import Workload
+    wl = Workload(f"store_{name}", B, H, D, tuple(segs), std=1.0, seed=5)
+    L = rc.Layout(list(segs), preset)
+    _, copy_wgs, copy_rows = L.prefill_plan(B, H, D)
+    total = B * H * L.rows(rc.ROWS_CACHED)
+    got = "store" if copy_wgs == 0 else ("tail" if copy_rows == total else "split")
+    assert got == regime, (copy_wgs, copy_rows, total)
+    check_request(wl, preset)
+    # every cache row is written: a poisoned cache comes back equal to the oracle's
+    inp = draw_inputs(wl)
+    q, k, v = (t.to(DEV) for t in inp.static)
+    nc = L.rows(rc.ROWS_CACHED)
+    kc = torch.full((B, H, nc, D), float("nan"), dtype=torch.bfloat16, device=DEV)
+    vc = torch.full_like(kc, float("-inf"))
+    rc.ref_kv_prefill(L, q, k, v, k_cache=kc, v_cache=vc, scale=wl.scale)
+    torch.cuda.synchronize()
+    _, _, _, kc_ref, vc_ref = oracle_prefill(inp, oracle_mask(inp, preset), wl.scale, rows=np.array([0]))
+    assert np.array_equal(f64(kc), kc_ref) and np.array_equal(f64(vc), vc_ref), "cache is not a bit copy"
+
+
 def test_ref1_request_40_steps():
     """Single-reference 1024^2 shape: 1 prefill + 40 steps with fresh live
     Q/K/V each step, all run over the one cache.  Steps 0, 19 and 39 are
