@@ -10,9 +10,9 @@
 // computes.  Dividing by a power of two is exact, so a code depends on x alone,
 // and code * s is exact in bf16.
 //
-// Five launches on the stream: amax accumulators cleared, per-(b, h) amax
+// Four launches on the stream: amax accumulators cleared, per-(b, h) amax
 // (work-group maxima, then one atomic max per work-group and tensor: the
-// result does not depend on the order), the quantising stores of K and of V,
+// result does not depend on the order), the quantising store of K and V,
 // and the scales written over the amax values.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -77,19 +77,31 @@ __global__ void fill_zero_kernel(float* a, int n) {
 }
 
 // Grid (B * H, ceil(n_cached / kRowsPerBlock)); 256 threads stride over the
-// block's rows x D/8 granules of K and V.
+// block's rows x D/8 granules of K and V, four granules of each in flight.
 __global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
   const int bh = blockIdx.x, b = bh / c.H, h = bh % c.H;
   const int gr = c.D / 8;
   const int row0 = blockIdx.y * kRowsPerBlock;
+  const int n = min(kRowsPerBlock, c.n_cached - row0) * gr;
   float mk = 0.f, mv = 0.f;
-  for (int g = threadIdx.x; g < kRowsPerBlock * gr; g += blockDim.x) {
-    const int pos = row0 + g / gr;
-    if (pos >= c.n_cached) break;
-    const int srow = source_row(c, pos);
-    const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + (g % gr) * 8;
-    mk = fmaxf(mk, amax8(*reinterpret_cast<const u32x4*>(c.k_src + off)));
-    mv = fmaxf(mv, amax8(*reinterpret_cast<const u32x4*>(c.v_src + off)));
+  for (int g0 = threadIdx.x; g0 < n; g0 += 4 * blockDim.x) {
+    u32x4 kx[4], vx[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int g = g0 + u * blockDim.x;
+      kx[u] = vx[u] = u32x4{0u, 0u, 0u, 0u};
+      if (g < n) {
+        const int srow = source_row(c, row0 + g / gr);
+        const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + (g % gr) * 8;
+        kx[u] = *reinterpret_cast<const u32x4*>(c.k_src + off);
+        vx[u] = *reinterpret_cast<const u32x4*>(c.v_src + off);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      mk = fmaxf(mk, amax8(kx[u]));
+      mv = fmaxf(mv, amax8(vx[u]));
+    }
   }
   __shared__ float red[2][256];
   red[0][threadIdx.x] = mk;
@@ -109,9 +121,9 @@ __global__ __launch_bounds__(256) void amax_kernel(const CacheStore8Params c) {
   }
 }
 
-// K8 or V8 (`which` 0 or 1): one thread per (b, h, cached row, granule of 8
-// elements).
-__global__ __launch_bounds__(256) void quant_kernel(const CacheStore8Params c, int which) {
+// K8 and V8: one thread per (b, h, cached row, granule of 8 elements) of
+// both tensors.
+__global__ __launch_bounds__(256) void quant_kernel(const CacheStore8Params c) {
   const int gr = c.D / 8;
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t total = int64_t(c.B) * c.H * c.n_cached * gr;
@@ -122,11 +134,12 @@ __global__ __launch_bounds__(256) void quant_kernel(const CacheStore8Params c, i
   const int64_t bh = rest / c.n_cached;
   const int b = int(bh / c.H), h = int(bh % c.H);
   const int srow = source_row(c, pos);
-  const uint16_t* src = which ? c.v_src : c.k_src;
-  uint8_t* dst = which ? c.v_dst : c.k_dst;
   const int64_t off = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
-  const u32x2 q = quant8(*reinterpret_cast<const u32x4*>(src + off), fp8_exponent(c.kv_scale[bh * 2 + which]));
-  *reinterpret_cast<u32x2*>(dst + (bh * c.n_cached + pos) * c.D + g * 8) = q;
+  const u32x4 kx = *reinterpret_cast<const u32x4*>(c.k_src + off);
+  const u32x4 vx = *reinterpret_cast<const u32x4*>(c.v_src + off);
+  const int64_t dof = (bh * c.n_cached + pos) * c.D + g * 8;
+  *reinterpret_cast<u32x2*>(c.k_dst + dof) = quant8(kx, fp8_exponent(c.kv_scale[bh * 2]));
+  *reinterpret_cast<u32x2*>(c.v_dst + dof) = quant8(vx, fp8_exponent(c.kv_scale[bh * 2 + 1]));
 }
 
 __global__ void finalize_scale_kernel(float* a, int n) {
@@ -144,8 +157,7 @@ int launch_cache_store_fp8(const CacheStore8Params& c, void* stream) {
   hipLaunchKernelGGL(amax_kernel, dim3(c.B * c.H, (c.n_cached + kRowsPerBlock - 1) / kRowsPerBlock), dim3(256), 0, s,
                      c);
   const int64_t tk = int64_t(c.B) * c.H * c.n_cached * (c.D / 8);
-  hipLaunchKernelGGL(quant_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c, 0);
-  hipLaunchKernelGGL(quant_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c, 1);
+  hipLaunchKernelGGL(quant_kernel, dim3((tk + 255) / 256), dim3(256), 0, s, c);
   hipLaunchKernelGGL(finalize_scale_kernel, dim3((nsc + 255) / 256), dim3(256), 0, s, c.kv_scale, nsc);
   return int(hipGetLastError());
 }
