@@ -1231,11 +1231,10 @@ __device__ __forceinline__ void attend_tile(const Params& p, const QSeg& qs, int
 // Copy work-group j of the prefill's cache store: rows [j R / C, (j + 1) R /
 // C) of the first R = c.rows flat cache rows ([B, H, n_cached] rows of D
 // values), D / 8 lanes per row, eight rows per lane in flight before their
-// stores.  Work-groups are dispatched in order, so these
-// start when the last attention work-groups have been placed and take the
-// CUs that the partial last round leaves free.  Loads and stores bypass the
-// caches' retention (the attention work-groups still running read their
-// keys through L2).
+// stores.  Work-groups are dispatched in order, so these start when the last
+// attention work-groups have been placed and take the CUs that the partial
+// last round leaves free.  Loads and stores bypass the caches' retention
+// (the attention work-groups still running read their keys through L2).
 template <int D>
 __device__ __forceinline__ void copy_tail(const CopyTail& c, int j, int tid) {
   constexpr int GR = D / 8, RPP = kThreads / GR, U = 8;
