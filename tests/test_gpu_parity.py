@@ -113,14 +113,20 @@ def test_ragged_segments(name, segs, preset, D):
 # at the end of the attention grid take every cached row ("tail"), the rows
 # that fit while the store kernel copies the rest ("split"), or none
 # ("store": the attention grid fills whole rounds).  Ragged segments, several
-# batch entries, one launch per batch entry (B = 2, H = 64), the paper mask.
+# batch entries, one launch per batch entry (B = 2, H = 64), the paper mask,
+# the largest segment table.
 RAGGED5 = [(0, 50), (1, 64), (2, 256), (3, 300), (3, 77)]
+# 32 segments, 30 of them cached (29 references of 39-300 tokens and the anchors)
+MANY = [(0, 40), (1, 32), (2, 128)] + [(3, n) for n in (
+    154, 99, 222, 275, 66, 39, 273, 165, 152, 131, 273, 276, 236, 110, 151, 110, 300, 232, 40, 65, 114, 54,
+    187, 48, 170, 275, 231, 251, 235)]
 CACHE_STORE = [
     ("tail_only", RAGGED5, "perref", 1, 8, 128, "tail"),
     ("split_ragged", RAGGED5, "perref", 3, 29, 128, "split"),
     ("split_per_batch", RAGGED5, "perref", 2, 64, 64, "split"),
     ("split_paper", RAGGED5, "paper", 1, 72, 64, "split"),
     ("store_only", [(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "perref", 2, 32, 64, "store"),
+    ("split_32_segments", MANY, "perref", 1, 13, 128, "split"),
 ]
 
 
