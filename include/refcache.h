@@ -227,6 +227,28 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
                             const void* q, const void* k, const void* v, int64_t tok_stride,
                             void* o, float* lse, void* stream);
 
+/* The same recompute (App. C's Base when L is dense over [LT, X, R]) with a
+ * workspace for the last-round split: when the grid of whole query tiles
+ * (one work-group each) fills more than the 256 CUs and its partial last
+ * round leaves enough of them idle, that round's T query tiles run as a long
+ * piece and a short piece of their keys each, and a merge kernel combines
+ * the two pieces' fp32 partials in a fixed order (the other tiles are
+ * computed whole, as rc_full_attention computes them).
+ *   workspace  device, 16-byte aligned, rc_full_workspace_bytes bytes, or
+ *              NULL: then the call is rc_full_attention.
+ * RC_ERR_WORKSPACE when a non-null workspace is misaligned or smaller than
+ * that size; other errors as rc_full_attention. */
+rc_status rc_full_attention_ws(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale,
+                               const void* q, const void* k, const void* v, int64_t tok_stride,
+                               void* o, float* lse, void* workspace, size_t ws_bytes, void* stream);
+
+/* Bytes of workspace rc_full_attention_ws uses: 2 * T * 512 * (D + 2) * 4 for
+ * the T query tiles of the partial last round it splits, 0 when it splits
+ * none (the grid fits one round or fills whole rounds, the idle CUs would
+ * run more than three rounds of short pieces, or a tile has fewer than 16 key
+ * tiles).  0 on invalid input. */
+size_t rc_full_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D);
+
 /* FP8 reference cache (the paper calls caching complementary to other
  * accelerations, Sec. 1 and Sec. 4.2; storing the cache in e4m3 halves its bytes,
  * its residency and the step's cached-key traffic).

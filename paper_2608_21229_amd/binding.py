@@ -70,6 +70,8 @@ SIGNATURES = {
                                                 _vp, _i32, _vp]),
     "rc_step_launch_shape": (_i32, [_PL, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i64),
                                     ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
+    "rc_full_attention_ws": (_i32, [_PL, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "rc_full_workspace_bytes": (_sz, [_PL, _i32, _i32, _i32]),
     "rc_prefill_launch_plan": (_i32, [_PL, _i32, _i32, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_i32),
                                       ctypes.POINTER(_i64)]),
     "rc_status_string": (ctypes.c_char_p, [_i32]),
@@ -152,6 +154,10 @@ class Layout:
         _check(lib().rc_step_launch_shape(ctypes.byref(self.c), B, H, D, splits, int(fp8), ctypes.byref(wg),
                                           ctypes.byref(bm), ctypes.byref(sp)))
         return wg.value, bm.value, sp.value
+
+    def full_workspace_bytes(self, B: int, H: int, D: int) -> int:
+        """Workspace of the full recompute's last-round split (0: no split)."""
+        return int(lib().rc_full_workspace_bytes(ctypes.byref(self.c), B, H, D))
 
     def prefill_plan(self, B: int, H: int, D: int):
         """(attention work-groups, copy work-groups, cache rows they copy) of
@@ -322,8 +328,11 @@ def step_masked_attention_noalloc(layout: Layout, q, k, v, k_cache, v_cache, o, 
 
 
 def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[float] = None,
-                   want_lse: bool = False, stream=None):
-    """Full recompute over all rows.  q/k/v: [B, N, H, D] bf16.  Returns (o, lse or None)."""
+                   want_lse: bool = False, last_round_split: bool = True, stream=None):
+    """Full recompute over all rows.  q/k/v: [B, N, H, D] bf16.  Returns (o, lse or None).
+    last_round_split: give the library the workspace it asks for to split the
+    grid's partial last round (rc_full_attention_ws); False computes every
+    query tile whole (rc_full_attention)."""
     torch = _torch()
     _rows_of(layout, q, ROWS_ALL, "full_attention")
     dev = _inputs(q, k, v)
@@ -337,9 +346,12 @@ def full_attention(layout: Layout, q, k, v, o=None, lse=None, scale: Optional[fl
     _expect(o, (B, N, H, D), "torch.bfloat16", "o")
     _expect(lse, (B, H, N), "torch.float32", "lse")
     _same_device(dev, o=o, lse=lse)
+    need = layout.full_workspace_bytes(B, H, D) if last_round_split else 0
     with torch.cuda.device(dev):
-        _check(lib().rc_full_attention(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
-                                       v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _stream(stream, dev)))
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device) if need else None
+        _check(lib().rc_full_attention_ws(ctypes.byref(layout.c), B, H, D, scale, q.data_ptr(), k.data_ptr(),
+                                          v.data_ptr(), ts, o.data_ptr(), _ptr(lse), _ptr(ws), need,
+                                          _stream(stream, dev)))
     return o, lse
 
 

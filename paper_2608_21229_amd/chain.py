@@ -141,10 +141,12 @@ class Chain:
 
         return self._run(h_live, rcb.ROWS_LIVE, attend, collect, stream=stream)
 
-    def full(self, h, collect: Optional[List] = None, stream=None):
+    def full(self, h, collect: Optional[List] = None, stream=None, last_round_split: bool = True):
         """h [B, N, H D]: every row in sequence order.  Returns the hidden state
-        after the last layer."""
+        after the last layer.  last_round_split=False computes every query tile
+        whole (bit-comparable with the cached path)."""
         def attend(l, q, k, v, o):
-            rcb.full_attention(self.layout, q, k, v, o=o, scale=self.scale, stream=stream)
+            rcb.full_attention(self.layout, q, k, v, o=o, scale=self.scale, last_round_split=last_round_split,
+                               stream=stream)
 
         return self._run(h, rcb.ROWS_ALL, attend, collect, stream=stream)

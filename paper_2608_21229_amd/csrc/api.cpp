@@ -515,9 +515,21 @@ rc_status rc_step_masked_attention_fp8(const rc_layout* L, int32_t B, int32_t H,
                    o_live, lse_live, splits, workspace, ws_bytes, stream);
 }
 
-rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q,
-                            const void* k, const void* v, int64_t tok_stride, void* o, float* lse,
-                            void* stream) {
+size_t rc_full_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D) {
+  using namespace rc;
+  if (B < 1 || H < 1 || (D != 64 && D != 128)) return 0;
+  if (check_layout(L, RC_ENTRY_FULL) != RC_OK) return 0;
+  Params p;
+  memset(&p, 0, sizeof p);
+  fill_common(p, B, H, 1.0f);
+  p.bm = rows_per_wg(kQBPlain);
+  if (plan(L, RC_ENTRY_FULL, p) != RC_OK) return 0;
+  return size_t(2) * last_round_tiles(p) * p.bm * size_t(D + 2) * sizeof(float);
+}
+
+rc_status rc_full_attention_ws(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q,
+                               const void* k, const void* v, int64_t tok_stride, void* o, float* lse,
+                               void* workspace, size_t ws_bytes, void* stream) {
   RC_TRY(check_layout(L, RC_ENTRY_FULL));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
@@ -541,8 +553,33 @@ rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D,
   p.o_sb = p.o_st * n;
   p.lse = lse;
   p.src[0] = bf16_source(k, v, tok_stride * n, D, tok_stride);
+  if (workspace) {
+    const int32_t T = last_round_tiles(p);
+    const size_t need = size_t(2) * T * p.bm * size_t(D + 2) * sizeof(float);
+    if (!aligned16(workspace) || ws_bytes < need) {
+      set_error("the last-round split needs a 16-byte aligned workspace of %zu bytes (got %zu)", need, ws_bytes);
+      return RC_ERR_WORKSPACE;
+    }
+    if (T > 0) {
+      p.splits = 2;
+      p.lr_tiles = T;
+      p.ws_o = static_cast<float*>(workspace);
+      p.ws_ml = p.ws_o + size_t(2) * T * p.bm * D;
+      RC_TRY(check_blocks(int64_t(B) * H * p.n_qtiles + T, "full attention"));
+      RC_TRY(hip_status(launch_attention(p, D, stream), "full attention launch"));
+      RC_TRY(hip_status(launch_combine_last_round(p, D, stream), "last-round merge launch"));
+      return RC_OK;
+    }
+    p.tail_num = 0;
+  }
   RC_TRY(hip_status(launch_attention(p, D, stream), "full attention launch"));
   return RC_OK;
+}
+
+rc_status rc_full_attention(const rc_layout* L, int32_t B, int32_t H, int32_t D, float scale, const void* q,
+                            const void* k, const void* v, int64_t tok_stride, void* o, float* lse,
+                            void* stream) {
+  return rc_full_attention_ws(L, B, H, D, scale, q, k, v, tok_stride, o, lse, nullptr, 0, stream);
 }
 
 rc_status rc_linear(int64_t M, int32_t N, int32_t K, const void* a, int64_t lda, const void* w, const void* r,

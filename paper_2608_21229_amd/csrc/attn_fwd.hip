@@ -1289,7 +1289,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
     }
   }
   int split, rest;
-  if (kSplit && p.tail_num > 0) {
+  if (kSplit && p.lr_tiles > 0) {
+    // last-round split: blocks [0, U) are whole query tiles (logical tiles
+    // [0, U)), then the long pieces of logical tiles [U, U + T), then their
+    // short pieces, which the CUs idle in the last round take first
+    const int T = p.lr_tiles, U = n_attn - 2 * T;
+    if (int(blockIdx.x) < U) {
+      split = -1;
+      rest = xcd_logical_block(blockIdx.x, U);
+    } else {
+      const int i = blockIdx.x - U;
+      split = i >= T;
+      rest = U + xcd_logical_block(i - split * T, T);
+    }
+  } else if (kSplit && p.tail_num > 0) {
     // tail split: blocks [0, Q) are the long pieces, dispatched first; blocks
     // [Q, 2 Q) the short ones.  Both halves map to query tiles the same way,
     // so (for Q a multiple of 8) a tile's short piece runs on the XCD of its
@@ -1302,6 +1315,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
     split = w % p.splits;
     rest = w / p.splits;
   }
+  const int w = rest;  // logical query tile
   const int t = rest % p.n_qtiles;
   rest /= p.n_qtiles;
   const int h = rest % p.H, b = rest / p.H;
@@ -1312,15 +1326,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(const Params p) {
   int kt_begin, kt_end;
   if (kSplit && p.tail_num > 0) {
     const int mid = int((int64_t(qs.ktiles) * p.tail_num) >> 10);
-    kt_begin = split ? mid : 0;
-    kt_end = split ? qs.ktiles : mid;
+    kt_begin = split > 0 ? mid : 0;
+    kt_end = split == 0 ? mid : qs.ktiles;
   } else {
     kt_begin = int(int64_t(qs.ktiles) * split / p.splits);
     kt_end = int(int64_t(qs.ktiles) * (split + 1) / p.splits);
   }
   int64_t part_row = -1;
-  if constexpr (kSplit)
-    part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * Blk<QB>::kRows;
+  if constexpr (kSplit) {
+    if (p.lr_tiles > 0) {
+      // piece s of last-round tile i: workspace rows (s T + i) BM + row
+      if (split >= 0) part_row = (int64_t(split) * p.lr_tiles + (w - (n_attn - 2 * p.lr_tiles))) * Blk<QB>::kRows;
+    } else {
+      part_row = ((int64_t(split) * p.B + b) * p.H + h) * p.n_rows + qs.row0 + (t - qs.tile0) * Blk<QB>::kRows;
+    }
+  }
   attend_tile<D, kF8, QB>(p, qs, t, b, h, kt_begin, kt_end, part_row, wave, lane);
 }
 
@@ -1422,6 +1442,38 @@ __global__ __launch_bounds__(256) void combine_balanced_kernel(const Params p, i
 
 // Split-KV merge: O = sum_s 2^(m_s - M) acc_s / sum_s 2^(m_s - M) l_s, in split order.
 // One thread per (row, 4 consecutive d).
+// Merge of one output row's split partials, in split order: partial s of the
+// row sits at workspace row r0 + s * stride (D floats of O, then max and sum
+// in the (max, sum) plane).  Writes 4 bf16 of O (columns 4 d4..) and, for
+// d4 = 0, the LSE when lse is not null.
+__device__ __forceinline__ void merge_partials(const float* ws_o, const float* ws_ml, int64_t r0, int64_t stride,
+                                               int splits, int D, int d4, uint16_t* op, float* lse) {
+  float M = -INFINITY;
+  for (int s = 0; s < splits; ++s) {
+    const float ls = ws_ml[(s * stride + r0) * 2 + 1];
+    if (ls > 0.f) M = fmaxf(M, ws_ml[(s * stride + r0) * 2]);
+  }
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float l = 0.f;
+  if (M != -INFINITY) {
+    for (int s = 0; s < splits; ++s) {
+      const float ls = ws_ml[(s * stride + r0) * 2 + 1];
+      if (!(ls > 0.f)) continue;
+      const float wgt = __builtin_amdgcn_exp2f(ws_ml[(s * stride + r0) * 2] - M);
+      const float4 o = *reinterpret_cast<const float4*>(ws_o + (s * stride + r0) * D + 4 * d4);
+      acc.x += wgt * o.x;
+      acc.y += wgt * o.y;
+      acc.z += wgt * o.z;
+      acc.w += wgt * o.w;
+      l += wgt * ls;
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  __bf16 o4[4] = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv), (__bf16)(acc.w * inv)};
+  *reinterpret_cast<u32x2*>(op) = __builtin_bit_cast(u32x2, o4);
+  if (lse && d4 == 0) *lse = l > 0.f ? M * 0.69314718055994531f + __logf(l) : -INFINITY;
+}
+
 __global__ __launch_bounds__(256) void combine_kernel(const CombineParams c) {
   const int dq = c.D / 4;
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -1433,32 +1485,33 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineParams c) {
   const int64_t bh = bhr / c.n_rows;
   const int h = int(bh % c.H), b = int(bh / c.H);
   const int64_t plane = int64_t(c.B) * c.H * c.n_rows;
-  float M = -INFINITY;
-  for (int s = 0; s < c.splits; ++s) {
-    const float ls = c.ws_ml[(s * plane + bhr) * 2 + 1];
-    if (ls > 0.f) M = fmaxf(M, c.ws_ml[(s * plane + bhr) * 2]);
-  }
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float l = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < c.splits; ++s) {
-      const float ls = c.ws_ml[(s * plane + bhr) * 2 + 1];
-      if (!(ls > 0.f)) continue;
-      const float wgt = __builtin_amdgcn_exp2f(c.ws_ml[(s * plane + bhr) * 2] - M);
-      const float4 o = *reinterpret_cast<const float4*>(c.ws_o + (s * plane + bhr) * c.D + 4 * d4);
-      acc.x += wgt * o.x;
-      acc.y += wgt * o.y;
-      acc.z += wgt * o.z;
-      acc.w += wgt * o.w;
-      l += wgt * ls;
-    }
-  }
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  __bf16 o4[4] = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv), (__bf16)(acc.w * inv)};
   uint16_t* op = c.o + int64_t(b) * c.o_sb + int64_t(row) * c.o_st + int64_t(h) * c.D + 4 * d4;
-  *reinterpret_cast<u32x2*>(op) = __builtin_bit_cast(u32x2, o4);
-  if (c.lse && d4 == 0)
-    c.lse[bhr] = l > 0.f ? M * 0.69314718055994531f + __logf(l) : -INFINITY;
+  merge_partials(c.ws_o, c.ws_ml, bhr, plane, c.splits, c.D, d4, op, c.lse ? c.lse + bhr : nullptr);
+}
+
+// Merge of the last-round split: one thread per 4 output elements of the
+// p.lr_tiles last query tiles (logical order); piece s of tile i holds row r
+// at workspace row (s T + i) BM + r.
+__global__ __launch_bounds__(256) void combine_last_round_kernel(const Params p, int D) {
+  const int dq = D / 4;
+  const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int T = p.lr_tiles;
+  if (idx >= int64_t(T) * p.bm * dq) return;
+  const int d4 = int(idx % dq);
+  const int64_t ir = idx / dq;
+  const int r = int(ir % p.bm), i = int(ir / p.bm);
+  const int64_t w = int64_t(p.B) * p.H * p.n_qtiles - T + i;
+  const int t = int(w % p.n_qtiles);
+  const int64_t bh = w / p.n_qtiles;
+  const int h = int(bh % p.H), b = int(bh / p.H);
+  int qi = 0;
+  while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
+  const int in_seg = (t - p.qseg[qi].tile0) * p.bm + r;
+  if (in_seg >= p.qseg[qi].len) return;
+  const int row = p.qseg[qi].row0 + in_seg;
+  uint16_t* op = p.o + int64_t(b) * p.o_sb + int64_t(row) * p.o_st + int64_t(h) * D + 4 * d4;
+  merge_partials(p.ws_o, p.ws_ml, int64_t(i) * p.bm + r, int64_t(T) * p.bm, 2, D, d4, op,
+                 p.lse ? p.lse + bh * p.n_rows + row : nullptr);
 }
 
 // Cache store: one thread per 16-byte granule of one cached (b, h, row),
@@ -1519,8 +1572,13 @@ int scratch_address(void** ptr) {
 
 int launch_attention(const Params& p, int D, void* stream) {
   const int64_t per_batch = int64_t(p.H) * p.n_qtiles * p.splits;
-  const int64_t blocks = int64_t(p.B) * per_batch;
+  // the last-round split adds one short piece per split tile
+  const int64_t blocks =
+      p.lr_tiles > 0 ? int64_t(p.B) * p.H * p.n_qtiles + p.lr_tiles : int64_t(p.B) * per_batch;
   if (blocks == 0) return 0;
+  if (p.lr_tiles < 0 || (p.lr_tiles > 0 && (p.splits != 2 || p.tail_num <= 0 || p.fp8 ||
+                                            p.lr_tiles > int64_t(p.B) * p.H * p.n_qtiles)))
+    return int(hipErrorInvalidValue);
   // copy work-groups ride on unsplit bf16 grids only (the other kernels have
   // no copy path)
   if (p.cp.blocks < 0 || (p.cp.blocks > 0 && (p.splits != 1 || p.fp8))) return int(hipErrorInvalidValue);
@@ -1571,6 +1629,14 @@ int launch_combine_balanced(const Params& p, int D, void* stream) {
   const int64_t total = int64_t(p.B) * p.H * p.n_rows * (D / 4);
   if (total == 0) return 0;
   hipLaunchKernelGGL(combine_balanced_kernel, dim3((total + 255) / 256), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), p, D);
+  return int(hipGetLastError());
+}
+
+int launch_combine_last_round(const Params& p, int D, void* stream) {
+  const int64_t total = int64_t(p.lr_tiles) * p.bm * (D / 4);
+  if (total == 0) return 0;
+  hipLaunchKernelGGL(combine_last_round_kernel, dim3((total + 255) / 256), dim3(256), 0,
                      static_cast<hipStream_t>(stream), p, D);
   return int(hipGetLastError());
 }

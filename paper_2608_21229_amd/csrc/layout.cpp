@@ -322,6 +322,29 @@ CopyPlan plan_copy_tail(const Params& p, int64_t n_cached) {
   return CopyPlan{int32_t(c), rows};
 }
 
+int32_t last_round_tiles(Params& p) {
+  // An unsplit grid of A > 256 whole query tiles leaves 256 - T CUs idle in
+  // its last round of T tiles.  Those T tiles run as a long piece (on the CUs
+  // the earlier rounds free) and a short piece (on the idle CUs, R rounds of
+  // them): the long piece takes R / (R + 1) of the keys so both end together,
+  // and the round shrinks to R / (R + 1) of a tile.  Kept to R <= 3 and to
+  // tiles of >= 16 key tiles, as the step's tail split (each piece pays a Q
+  // load, a partial write and its share of the merge).
+  const int64_t A = int64_t(p.B) * p.H * p.n_qtiles;
+  const int64_t T = A % kCUs, idle = kCUs - T;
+  if (A <= kCUs || T == 0) return 0;
+  const int64_t r = (T + idle - 1) / idle;
+  if (r > 3) return 0;
+  for (int64_t w = A - T; w < A; ++w) {
+    const int t = int(w % p.n_qtiles);
+    int qi = 0;
+    while (qi + 1 < p.n_qseg && p.qseg[qi + 1].tile0 <= t) ++qi;
+    if (p.qseg[qi].ktiles < 16) return 0;
+  }
+  p.tail_num = int32_t(1024 * r / (r + 1));
+  return int32_t(T);
+}
+
 int32_t tail_num(const Params& p) {
   // Q query tiles on Q CUs; 256 - Q CUs run the short pieces, R rounds each:
   // the long piece takes R / (R + 1) of the keys so both end together.

@@ -96,6 +96,8 @@ struct Params {
   int32_t B, H, n_rows, n_qseg, n_qtiles, splits;  // splits: kSplitsBalanced = balanced schedule
   int32_t bm;          // query rows per work-group tile (rows_per_wg of the kernel that runs)
   int32_t tail_num;    // tail split (splits = 2): split 0 takes floor(ktiles * tail_num / 1024) key tiles; 0 = even
+  int32_t lr_tiles;    // last-round split (splits = 2, tail_num > 0): only the last lr_tiles query tiles
+                       // (logical order) run as a long and a short piece; the others whole, written directly
   int32_t fp8;         // key source 1 is the FP8 cache
   const float* kv_scale;  // FP8 cache: [B, H, 2] power-of-two scales of K and V
   int64_t units_bh;    // key-tile units (query tile x key tile) per (batch, head)
@@ -170,6 +172,9 @@ int64_t count_cached_rows(const rc_layout* L);
 rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first = false);
 int32_t auto_splits(const Params& p);
 int32_t tail_num(const Params& p);  // the long split's share of the key tiles, in 1/1024
+// The full recompute's last-round split: the query tiles of an unsplit grid's
+// partial last round (0 when none pays), with p.tail_num set for them.
+int32_t last_round_tiles(Params& p);
 // The prefill's bf16 cache store: the copy work-groups appended to the
 // attention grid and the flat cache rows [0, rows) they take; the store
 // kernel copies the rest.
@@ -187,6 +192,7 @@ void set_error(const char* fmt, ...);
 bool per_batch_launches(const Params& p);
 int launch_attention(const Params& p, int D, void* stream);
 int launch_combine(const CombineParams& c, void* stream);
+int launch_combine_last_round(const Params& p, int D, void* stream);  // the lr_tiles tiles' partials
 int launch_attention_balanced(const Params& p, int D, void* stream);
 int launch_combine_balanced(const Params& p, int D, void* stream);
 int launch_cache_store(const CacheStoreParams& c, void* stream);

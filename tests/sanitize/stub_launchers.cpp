@@ -99,6 +99,11 @@ namespace rc {
 
 int launch_attention(const Params& p, int D, void*) {
   check_params(p, D, false);
+  REQUIRE(p.lr_tiles >= 0 && p.lr_tiles < kCUs, p.lr_tiles, 0);
+  if (p.lr_tiles > 0) {
+    REQUIRE(p.splits == 2 && p.tail_num > 0 && !p.fp8 && p.cp.blocks == 0, p.splits, p.tail_num);
+    REQUIRE(p.lr_tiles <= int64_t(p.B) * p.H * p.n_qtiles, p.lr_tiles, p.n_qtiles);
+  }
   const CopyTail& c = p.cp;
   REQUIRE(c.blocks >= 0 && c.blocks < kCUs, c.blocks, 0);
   if (c.blocks > 0) {
@@ -121,6 +126,13 @@ int launch_attention_balanced(const Params& p, int D, void*) {
 
 int launch_combine_balanced(const Params& p, int D, void*) {
   check_params(p, D, true);
+  ++g_launches;
+  return 0;
+}
+
+int launch_combine_last_round(const Params& p, int D, void*) {
+  check_params(p, D, false);
+  REQUIRE(p.lr_tiles > 0 && p.splits == 2 && p.ws_o && p.ws_ml, p.lr_tiles, p.splits);
   ++g_launches;
   return 0;
 }

@@ -109,6 +109,11 @@ def _full(L, B=1, H=2, D=128, scale=0.1, q=FAKE, k=FAKE, v=FAKE, ts=None, o=FAKE
     return rc.lib().rc_full_attention(ctypes.byref(L.c), B, H, D, scale, q, k, v, ts, o, lse, None)
 
 
+def _full_ws(L, B=1, H=2, D=128, scale=0.1, q=FAKE, k=FAKE, v=FAKE, ts=None, o=FAKE, lse=None, ws=None, wsb=0):
+    ts = H * D if ts is None else ts
+    return rc.lib().rc_full_attention_ws(ctypes.byref(L.c), B, H, D, scale, q, k, v, ts, o, lse, ws, wsb, None)
+
+
 SEGS = [(0, 8), (1, 16), (2, 64), (3, 64)]
 
 
@@ -262,6 +267,38 @@ def test_step_launch_shape():
     wg, bm, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
     assert rc.lib().rc_step_launch_shape(ctypes.byref(L.c), 1, 2, 128, 0, 0, None, ctypes.byref(bm),
                                          ctypes.byref(sp)) == rc.RC_ERR_ARG
+
+
+def test_full_last_round_split_workspace():
+    """rc_full_workspace_bytes: 2 T 512 (D + 2) 4 bytes for the T query tiles
+    of the grid's partial last round, when the idle CUs run at most three
+    rounds of short pieces and every split tile has >= 16 key tiles."""
+    # the dense Base over [LT, X, R] at five references: 49 tiles x 24 heads =
+    # 1176 work-groups, T = 152 on 104 idle CUs (two rounds of short pieces)
+    Lb = rc.Layout([(1, 512), (2, 4096)] + [(3, 4096)] * 5, "dense")
+    assert Lb.full_workspace_bytes(1, 24, 128) == 2 * 152 * 512 * 130 * 4
+    # B = 2: 2352 work-groups, T = 48
+    assert Lb.full_workspace_bytes(2, 24, 128) == 2 * 48 * 512 * 130 * 4
+    # one round or whole rounds: nothing to split
+    assert Lb.full_workspace_bytes(1, 4, 128) == 0          # 196 work-groups
+    L2 = rc.Layout([(1, 512), (2, 3584)], "dense")           # 8 tiles per head
+    assert L2.full_workspace_bytes(1, 64, 64) == 0           # 512 work-groups
+    # 36 heads: 1764 work-groups, 228 tiles in the last round on 28 idle CUs
+    # (nine rounds of short pieces): not split
+    assert Lb.full_workspace_bytes(1, 36, 128) == 0
+    # the per-reference mask's anchor tiles (one key tile) in the last round: not split
+    Lp = rc.Layout([(0, 64), (1, 512), (2, 4096)] + [(3, 4096)] * 5, "perref")
+    assert Lp.full_workspace_bytes(1, 24, 128) == 0
+    for kw in (dict(D=96), dict(B=0), dict(H=0)):
+        args = dict(B=1, H=24, D=128)
+        args.update(kw)
+        assert Lb.full_workspace_bytes(args["B"], args["H"], args["D"]) == 0
+    # a workspace that is too small or misaligned is refused before any launch;
+    # none at all runs the unsplit recompute
+    need = Lb.full_workspace_bytes(1, 24, 128)
+    W = rc.RC_ERR_WORKSPACE
+    assert _full_ws(Lb, H=24, ws=FAKE, wsb=need - 1) == W
+    assert _full_ws(Lb, H=24, ws=FAKE + 4, wsb=need) == W
 
 
 def test_prefill_launch_plan():

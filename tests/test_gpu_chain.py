@@ -271,7 +271,7 @@ def test_chain_cached_path_equals_full_recompute_bitwise(case):
     hs_step, hs_full = [], []
     ch.step(h_l, caches, splits=1, collect=hs_step)
     h0 = assemble(wl, h_s, h_l)
-    ch.full(h0, collect=hs_full)
+    ch.full(h0, collect=hs_full, last_round_split=False)
     torch.cuda.synchronize()
     live = seq_index(wl, False).to(DEV)
     cached_segs = om.cached_segments(wl.kinds, om.perref_mask(wl.kinds))

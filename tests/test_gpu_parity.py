@@ -152,6 +152,65 @@ def test_prefill_cache_store_forms(name, segs, preset, B, H, D, regime):
     assert np.array_equal(f64(kc), kc_ref) and np.array_equal(f64(vc), vc_ref), "cache is not a bit copy"
 
 
+def last_round_rows(lens, B, H, bm=512, cus=256):
+    """[B, N, H] bool: the (batch, row, head) cells of the query tiles the
+    full recompute's last-round split runs as two pieces -- the last
+    (B H tiles) mod 256 tiles in (batch, head, tile) order, tiles of bm rows
+    inside each segment."""
+    tiles, r0 = [], 0
+    for n in lens:
+        tiles += [(r0 + s, min(bm, n - s)) for s in range(0, n, bm)]
+        r0 += n
+    nt, A = len(tiles), B * H * len(tiles)
+    m = torch.zeros((B, r0, H), dtype=torch.bool, device=DEV)
+    for w in range(A - A % cus, A):
+        b, h, t = w // (H * nt), (w // nt) % H, w % nt
+        m[b, tiles[t][0]:tiles[t][0] + tiles[t][1], h] = True
+    return m
+
+
+# The full recompute's last-round split (rc_full_attention_ws): grids of whole
+# query tiles whose partial last round leaves CUs idle; ragged last tiles,
+# several query segments with different key counts, B = 2 and 3.
+LAST_ROUND = [
+    ("dense_D64", [(1, 100), (2, 1000), (3, 1500)], "dense", 1, 48, 64),
+    ("paper_B2", [(1, 100), (2, 1000), (3, 1500), (3, 777)], "paper", 2, 24, 128),
+    ("dense_B3", [(1, 100), (2, 1000), (3, 1500), (3, 777)], "dense", 3, 16, 64),
+]
+
+
+@pytest.mark.parametrize("name,segs,preset,B,H,D", LAST_ROUND)
+def test_full_recompute_last_round_split(name, segs, preset, B, H, D):
+    from synthgen import Workload
+    wl = Workload(f"lastround_{name}", B, H, D, tuple(segs), std=1.0, seed=9)
+    print(f"[case] last-round split {name}: B={B} H={H} D={D} segments={segs} mask={preset}", flush=True)
+    L = rc.Layout(list(segs), preset)
+    assert L.full_workspace_bytes(B, H, D) > 0
+    inp = draw_inputs(wl)
+    q, k, v = (full_sequence(inp, i).to(DEV) for i in range(3))
+    o, lse = rc.full_attention(L, q, k, v, scale=wl.scale, want_lse=True)
+    o2, lse2 = rc.full_attention(L, q, k, v, scale=wl.scale, want_lse=True)
+    ou, lseu = rc.full_attention(L, q, k, v, scale=wl.scale, want_lse=True, last_round_split=False)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2) and torch.equal(lse, lse2), "split recompute is not deterministic"
+    N = q.shape[1]
+    rows = sample_rows(N, 5, seed=1)
+    O, ls, _ = oa.full_attention(inp.kinds, inp.lens, om.PRESETS[preset](inp.kinds), *(f64(t) for t in (q, k, v)),
+                                 wl.scale, rows=rows)
+    check(o, O, f"{name} split O", rows)
+    check_lse(lse, ls, f"{name} split", rows)
+    split = last_round_rows(list(inp.lens), B, H)
+    assert split.any() and not split.all()
+    assert torch.equal(o[~split], ou[~split]), "tiles outside the last round differ from the unsplit call"
+    assert torch.equal(lse.permute(0, 2, 1)[~split], lseu.permute(0, 2, 1)[~split])
+    # the split tiles: every row of them against the oracle
+    srows = np.nonzero(split.any(dim=2).any(dim=0).cpu().numpy())[0]
+    O2, ls2, _ = oa.full_attention(inp.kinds, inp.lens, om.PRESETS[preset](inp.kinds),
+                                   *(f64(t) for t in (q, k, v)), wl.scale, rows=srows)
+    check(o, O2, f"{name} split rows O", srows)
+    check_lse(lse, ls2, f"{name} split rows", srows)
+
+
 def test_ref1_request_40_steps():
     """Single-reference 1024^2 shape: 1 prefill + 40 steps with fresh live
     Q/K/V each step, all run over the one cache.  Steps 0, 19 and 39 are
@@ -224,7 +283,7 @@ def test_batch_entries_equal_single_calls():
     qa, ka, va = (full_sequence(inp, i).to(DEV) for i in range(3))
     o2, l2, kc2, vc2 = rc.ref_kv_prefill(L, qs, ks, vs, scale=wl.scale, want_lse=True)
     s2, sl2 = rc.step_masked_attention(L, ql, kl, vl, kc2, vc2, scale=wl.scale, splits=1, want_lse=True)
-    f2, fl2 = rc.full_attention(L, qa, ka, va, scale=wl.scale, want_lse=True)
+    f2, fl2 = rc.full_attention(L, qa, ka, va, scale=wl.scale, want_lse=True, last_round_split=False)
     for b in range(2):
         sl = slice(b, b + 1)
         o1, l1, kc1, vc1 = rc.ref_kv_prefill(L, qs[sl].contiguous(), ks[sl].contiguous(), vs[sl].contiguous(),
@@ -232,7 +291,7 @@ def test_batch_entries_equal_single_calls():
         s1, sl1 = rc.step_masked_attention(L, ql[sl].contiguous(), kl[sl].contiguous(), vl[sl].contiguous(),
                                            kc1, vc1, scale=wl.scale, splits=1, want_lse=True)
         f1, fl1 = rc.full_attention(L, qa[sl].contiguous(), ka[sl].contiguous(), va[sl].contiguous(),
-                                    scale=wl.scale, want_lse=True)
+                                    scale=wl.scale, want_lse=True, last_round_split=False)
         torch.cuda.synchronize()
         for name, x2, x1 in (("prefill O", o2, o1), ("prefill LSE", l2, l1), ("K cache", kc2, kc1),
                              ("V cache", vc2, vc1), ("step O", s2, s1), ("step LSE", sl2, sl1),
@@ -248,7 +307,7 @@ def test_ref5_full_recompute_and_step_rows():
     inp = draw_inputs(wl)
     q, k, v = (full_sequence(inp, i).to(DEV) for i in range(3))
     L = layout_for(inp, "perref")
-    of, _ = rc.full_attention(L, q, k, v, scale=wl.scale)
+    of, _ = rc.full_attention(L, q, k, v, scale=wl.scale, last_round_split=False)
     o, _, kc, vc = run_prefill(L, inp, wl.scale, want_lse=False)
     ol, _ = run_step(L, inp, kc, vc, wl.scale, splits=1, want_lse=False)
     torch.cuda.synchronize()
@@ -262,12 +321,17 @@ def test_ref5_full_recompute_and_step_rows():
     kinds, lens = inp.kinds[1:], inp.lens[1:]
     LB = rc.Layout(list(zip(kinds, lens)), "dense")
     qb, kb, vb = q[:, 64:].contiguous(), k[:, 64:].contiguous(), v[:, 64:].contiguous()
+    assert LB.full_workspace_bytes(1, wl.H, wl.D) > 0   # the Base runs with the last-round split
     ob, _ = rc.full_attention(LB, qb, kb, vb, scale=wl.scale)
+    obu, _ = rc.full_attention(LB, qb, kb, vb, scale=wl.scale, last_round_split=False)
     torch.cuda.synchronize()
     rows = sample_rows(qb.shape[1], 101)
     O, _, _ = oa.full_attention(kinds, lens, om.dense_mask(kinds), *(f64(t) for t in (qb, kb, vb)), wl.scale,
                                 rows=rows)
     check(ob, O, "ref5 full dense base", rows)
+    check(obu, O, "ref5 full dense base, unsplit", rows)
+    keep = ~last_round_rows(lens, 1, wl.H)
+    assert torch.equal(ob[keep], obu[keep]), "tiles outside the last round differ from the unsplit call"
 
 
 @pytest.mark.parametrize("preset", ["perref", "paper"])
