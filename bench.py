@@ -556,6 +556,8 @@ def main():
         "roofline": {
             "kernel": (f"attn_fwd_kernel<{D}, false, {f8}>" if step_splits == 1
                        else f"attn_fwd_balanced_kernel<{D}> + combine_balanced_kernel" if step_splits == rc.SPLITS_BALANCED
+                       else f"attn_fwd_kernel<{D}, true, {f8}> + combine_last_round_kernel"
+                       if step_splits == rc.SPLITS_LAST_ROUND
                        else f"attn_fwd_kernel<{D}, true, {f8}> + combine_kernel"),
             "bound": "mfma",
             "achieved": achieved,

@@ -81,6 +81,17 @@ extern "C" {
  * fill more than half the CUs and R <= 3 (Q <= 192). */
 #define RC_SPLITS_TAIL (-2)
 
+/* `splits` value of rc_step_masked_attention for the last-round split: when
+ * the query tiles (one work-group each) outnumber the 256 CUs and the last
+ * round of T tiles leaves 256 - T of them idle, those T tiles run as a long
+ * and a short piece of their keys as in RC_SPLITS_TAIL (R = ceil(T / (256 -
+ * T)) <= 3 rounds of short pieces on the idle CUs; every split tile has at
+ * least 16 key tiles), and the other tiles run whole, written directly.
+ * Workspace 2 * T * 512 * (D + 2) * 4 bytes (rc_step_workspace_bytes); where
+ * it does not apply the step runs unsplit and needs none.
+ * rc_step_auto_splits returns it for such grids. */
+#define RC_SPLITS_LAST_ROUND (-3)
+
 typedef enum {
   RC_OK = 0,
   RC_ERR_ARG = -1,                 /* null/misaligned pointer, bad size or stride */
@@ -154,23 +165,28 @@ int64_t rc_rows(const rc_layout* L, int32_t which);
 
 /* Bytes of fp32 workspace rc_step_masked_attention needs for `splits`
  * key splits (0 when splits == 1): splits * B * H * N_live * (D + 2) * 4,
- * two splits' worth for RC_SPLITS_TAIL, and the fixed size given above for
+ * two splits' worth for RC_SPLITS_TAIL, the last round's pieces for
+ * RC_SPLITS_LAST_ROUND (above), and the fixed size given above for
  * RC_SPLITS_BALANCED.  splits = 0 resolves the automatic choice first.
  * 0 on invalid input. */
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits);
 
-/* The split count rc_step_masked_attention uses when passed splits = 0: 1
- * when the query tiles fill more than 192 CUs, RC_SPLITS_TAIL when they fill
- * more than half, otherwise as many even splits as keep one round of work-groups (at
- * most one per 8 key tiles and 32 in all). */
+/* The split count rc_step_masked_attention uses when passed splits = 0:
+ * RC_SPLITS_LAST_ROUND when the query tiles outnumber the 256 CUs and that
+ * split applies, 1 when they fill more than 192 CUs otherwise,
+ * RC_SPLITS_TAIL when they fill more than half, otherwise as many even splits
+ * as keep one round of work-groups (at most one per 8 key tiles and 32 in
+ * all). */
 int32_t rc_step_auto_splits(const rc_layout* L, int32_t B, int32_t H, int32_t D);
 
 /* Launch shape of the step's attention kernel for `splits` (0 = automatic)
  * with the bf16 cache (fp8 = 0) or the FP8 cache (fp8 = 1), for occupancy
  * reports: *work_groups over all its launches (one per query tile and split;
- * 256 for RC_SPLITS_BALANCED), *rows_per_wg the query rows per work-group,
- * *splits_used the split count it resolves to (2 for the tail split, 1 where
- * the FP8 step drops it, RC_SPLITS_BALANCED for the balanced schedule).
+ * the whole tiles plus two per split tile for RC_SPLITS_LAST_ROUND; 256 for
+ * RC_SPLITS_BALANCED), *rows_per_wg the query rows per work-group,
+ * *splits_used the split count it resolves to (2 for the tail split,
+ * RC_SPLITS_LAST_ROUND when that split applies and 1 when it does not,
+ * RC_SPLITS_BALANCED for the balanced schedule).
  * Host only; RC_ERR_ARG on bad arguments or null outputs, RC_ERR_UNSUPPORTED
  * for head_dim other than 64/128 and for the balanced schedule with the FP8
  * cache. */
@@ -211,7 +227,8 @@ rc_status rc_ref_kv_prefill(const rc_layout* L, int32_t B, int32_t H, int32_t D,
  *   o_live                  [B, N_live, H, D] out;  lse_live [B, H, N_live] fp32, nullable.
  *   splits                  key splits per query tile (split-KV); 0 = automatic,
  *                           1 = none, 2..32 even splits, RC_SPLITS_TAIL,
- *                           RC_SPLITS_BALANCED.  Anything but 1 needs
+ *                           RC_SPLITS_BALANCED, RC_SPLITS_LAST_ROUND.  Any
+ *                           choice with a nonzero rc_step_workspace_bytes needs
  *                           `workspace` (device, 16-byte aligned) of
  *                           rc_step_workspace_bytes bytes; partials are merged
  *                           in a fixed order. */

@@ -16,7 +16,7 @@ from .binding import (  # noqa: F401
     SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF,
     MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE, MASKS,
     ENTRY_PREFILL, ENTRY_STEP, ENTRY_FULL,
-    ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL, SPLITS_BALANCED, SPLITS_TAIL,
+    ROWS_STATIC, ROWS_LIVE, ROWS_CACHED, ROWS_ALL, SPLITS_BALANCED, SPLITS_TAIL, SPLITS_LAST_ROUND,
     RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP,
 )
 from .chain import Chain  # noqa: F401,E402

@@ -18,6 +18,7 @@ RC_MAX_SEGMENTS = 32
 SPLITS_BALANCED = -1   # rc_step_masked_attention: one round of 256 work-groups sharing all key tiles evenly
 NOALLOC_SCRATCH_BYTES = 128 << 20   # rc_step_masked_attention_noalloc's static scratch per GPU
 SPLITS_TAIL = -2       # rc_step_masked_attention: a long and a short key split per query tile (idle CUs take the short)
+SPLITS_LAST_ROUND = -3  # rc_step_masked_attention: the tail split for the query tiles of a grid's partial last round
 RC_OK, RC_ERR_ARG, RC_ERR_UNSUPPORTED, RC_ERR_MASK_NOT_CACHEABLE, RC_ERR_WORKSPACE, RC_ERR_HIP = 0, -1, -2, -3, -4, -5
 SEG_ANCHOR, SEG_TEXT, SEG_TARGET, SEG_REF = 0, 1, 2, 3
 MASK_PAPER, MASK_PERREF, MASK_ISOLATED, MASK_DENSE = 0, 1, 2, 3
@@ -270,8 +271,9 @@ def step_masked_attention(layout: Layout, q, k, v, k_cache, v_cache, o=None, lse
                           workspace=None, scale: Optional[float] = None, want_lse: bool = False, stream=None):
     """Per-step attention.  q/k/v: [B, N_live, H, D] bf16 (LT and X tokens);
     k_cache/v_cache: [B, H, N_cached, D].  splits: 0 automatic, 1 none, > 1
-    even split-KV, SPLITS_TAIL the tail split, SPLITS_BALANCED the balanced
-    schedule.  Returns (o, lse or None)."""
+    even split-KV, SPLITS_TAIL the tail split, SPLITS_LAST_ROUND the tail split
+    of the last round's tiles, SPLITS_BALANCED the balanced schedule.  Returns
+    (o, lse or None)."""
     torch = _torch()
     _rows_of(layout, q, ROWS_LIVE, "step_masked_attention")
     dev = _inputs(q, k, v)

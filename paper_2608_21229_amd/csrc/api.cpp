@@ -262,6 +262,9 @@ rc_status plan_step(const rc_layout* L, int32_t D, bool fp8, int32_t splits, Par
   if (splits == kSplitsTail) {
     p.splits = 2;
     p.tail_num = tail_num(p);
+  } else if (splits == kSplitsLastRound) {
+    p.lr_tiles = last_round_tiles(p);
+    p.splits = p.lr_tiles > 0 ? 2 : 1;
   } else {
     p.splits = splits;
   }
@@ -282,9 +285,10 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   RC_TRY(check_layout(L, RC_ENTRY_STEP));
   RC_TRY(check_dims(B, H, D, scale));
   RC_TRY(check_stride(tok_stride, H, D));
-  if (splits < kSplitsTail || splits > kMaxSplits) {
-    set_error("splits = %d must be RC_SPLITS_TAIL (-2), RC_SPLITS_BALANCED (-1) or in [0, %d]", splits,
-              kMaxSplits);
+  if (splits < kSplitsLastRound || splits > kMaxSplits) {
+    set_error("splits = %d must be RC_SPLITS_LAST_ROUND (-3), RC_SPLITS_TAIL (-2), RC_SPLITS_BALANCED (-1) or in "
+              "[0, %d]",
+              splits, kMaxSplits);
     return RC_ERR_ARG;
   }
   const int64_t n_live = count_rows(L, RowSet::Live);
@@ -363,7 +367,8 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
       return RC_ERR_WORKSPACE;
     }
     p.ws_o = static_cast<float*>(workspace);
-    p.ws_ml = p.ws_o + size_t(p.splits) * B * H * n_live * D;
+    p.ws_ml = p.lr_tiles > 0 ? p.ws_o + size_t(2) * p.lr_tiles * p.bm * D
+                             : p.ws_o + size_t(p.splits) * B * H * n_live * D;
     c.ws_o = p.ws_o;
     c.ws_ml = p.ws_ml;
     c.o = p.o;
@@ -378,8 +383,10 @@ rc_status step_impl(const rc_layout* L, int32_t B, int32_t H, int32_t D, float s
   }
   // combine: one thread per 4 output elements, 256 per work-group
   if (p.splits > 1) RC_TRY(check_blocks((int64_t(B) * H * n_live * (D / 4) + 255) / 256, "split-KV combine"));
+  if (p.lr_tiles > 0) RC_TRY(check_blocks(int64_t(B) * H * p.n_qtiles + p.lr_tiles, "step attention"));
   RC_TRY(hip_status(launch_attention(p, D, stream), "step attention launch"));
-  if (p.splits > 1) RC_TRY(hip_status(launch_combine(c, stream), "split-KV combine launch"));
+  if (p.lr_tiles > 0) RC_TRY(hip_status(launch_combine_last_round(p, D, stream), "last-round merge launch"));
+  else if (p.splits > 1) RC_TRY(hip_status(launch_combine(c, stream), "split-KV combine launch"));
   return RC_OK;
 }
 
@@ -448,7 +455,7 @@ rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t
     return RC_ERR_ARG;
   }
   RC_TRY(check_dims(B, H, D, 1.0f));
-  if (splits < kSplitsTail || splits > kMaxSplits || (fp8 != 0 && fp8 != 1)) {
+  if (splits < kSplitsLastRound || splits > kMaxSplits || (fp8 != 0 && fp8 != 1)) {
     set_error("rc_step_launch_shape: splits = %d or fp8 = %d out of range", splits, fp8);
     return RC_ERR_ARG;
   }
@@ -463,15 +470,27 @@ rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t
   RC_TRY(plan_step(L, D, fp8 != 0, splits, p));
   *rows_per_wg = p.bm;
   *splits_used = p.splits;
-  *work_groups = p.splits == kSplitsBalanced ? int64_t(p.bal_wgs) : int64_t(B) * H * p.n_qtiles * p.splits;
+  if (p.lr_tiles > 0) *splits_used = kSplitsLastRound;
+  *work_groups = p.splits == kSplitsBalanced ? int64_t(p.bal_wgs)
+                 : p.lr_tiles > 0            ? int64_t(B) * H * p.n_qtiles + p.lr_tiles
+                                             : int64_t(B) * H * p.n_qtiles * p.splits;
   return RC_OK;
 }
 
 size_t rc_step_workspace_bytes(const rc_layout* L, int32_t B, int32_t H, int32_t D, int32_t splits) {
   if (check_layout(L, RC_ENTRY_STEP) != RC_OK) return 0;
-  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsTail || splits > kMaxSplits) return 0;
+  if (B < 1 || H < 1 || (D != 64 && D != 128) || splits < kSplitsLastRound || splits > kMaxSplits) return 0;
   if (splits == 0) splits = rc_step_auto_splits(L, B, H, D);
   if (splits == kSplitsBalanced) return balanced_workspace_bytes(D);
+  if (splits == kSplitsLastRound) {
+    Params p;
+    memset(&p, 0, sizeof p);
+    p.B = B;
+    p.H = H;
+    p.bm = rows_per_wg(kQBPlain);
+    if (plan(L, RC_ENTRY_STEP, p) != RC_OK) return 0;
+    return size_t(2) * last_round_tiles(p) * p.bm * size_t(D + 2) * sizeof(float);
+  }
   if (splits == kSplitsTail) splits = 2;
   if (splits <= 1) return 0;
   const int64_t n_live = count_rows(L, RowSet::Live);

@@ -1576,8 +1576,8 @@ int launch_attention(const Params& p, int D, void* stream) {
   const int64_t blocks =
       p.lr_tiles > 0 ? int64_t(p.B) * p.H * p.n_qtiles + p.lr_tiles : int64_t(p.B) * per_batch;
   if (blocks == 0) return 0;
-  if (p.lr_tiles < 0 || (p.lr_tiles > 0 && (p.splits != 2 || p.tail_num <= 0 || p.fp8 ||
-                                            p.lr_tiles > int64_t(p.B) * p.H * p.n_qtiles)))
+  if (p.lr_tiles < 0 ||
+      (p.lr_tiles > 0 && (p.splits != 2 || p.tail_num <= 0 || p.lr_tiles > int64_t(p.B) * p.H * p.n_qtiles)))
     return int(hipErrorInvalidValue);
   // copy work-groups ride on unsplit bf16 grids only (the other kernels have
   // no copy path)

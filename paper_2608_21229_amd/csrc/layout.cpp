@@ -228,7 +228,8 @@ rc_status plan(const rc_layout* L, int32_t entry, Params& p, bool fresh_first) {
 }
 
 int32_t auto_splits(const Params& p) {
-  // Split the keys only when the query tiles alone leave CUs idle.  When they
+  // Beyond one round of query tiles, the last-round split (when it applies).
+  // Otherwise split the keys only when the query tiles alone leave CUs idle.  When they
   // fill more than half of the 256 CUs, the tail split uses the rest: every
   // query tile keeps one work-group for most of its keys and the short
   // remainders run on the idle CUs, R = ceil(Q / (256 - Q)) in turn.  Each
@@ -239,7 +240,12 @@ int32_t auto_splits(const Params& p) {
   // Keep >= 8 key tiles per split.
   const int64_t wgs = int64_t(p.B) * p.H * p.n_qtiles;
   const int64_t slots = 256;  // one work-group per CU
-  if (wgs <= 0 || wgs >= slots) return 1;
+  if (wgs <= 0) return 1;
+  if (wgs >= slots) {
+    // more tiles than CUs: split only the partial last round's tiles
+    Params q = p;
+    return last_round_tiles(q) > 0 ? kSplitsLastRound : 1;
+  }
   int max_kt = 0;
   for (int i = 0; i < p.n_qseg; ++i)
     if (p.qseg[i].ktiles > max_kt) max_kt = p.qseg[i].ktiles;

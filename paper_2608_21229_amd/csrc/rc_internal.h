@@ -35,6 +35,7 @@ constexpr int kMaxSplits = 32;
 constexpr int kBalancedWGs = 256;
 constexpr int32_t kSplitsBalanced = RC_SPLITS_BALANCED;
 constexpr int32_t kSplitsTail = RC_SPLITS_TAIL;
+constexpr int32_t kSplitsLastRound = RC_SPLITS_LAST_ROUND;
 
 struct KeyRange {
   int32_t start;   // first key token inside its source

@@ -45,7 +45,7 @@ def test_random_layouts_through_every_entry(preset):
             assert _prefill(L, B=B, H=H, D=D, ts=ts) == rc.RC_ERR_MASK_NOT_CACHEABLE
             continue
         assert _prefill(L, B=B, H=H, D=D, ts=ts, lse=FAKE) == rc.RC_OK
-        for splits in (1, 2, 5, 0, rc.SPLITS_TAIL, rc.SPLITS_BALANCED):
+        for splits in (1, 2, 5, 0, rc.SPLITS_TAIL, rc.SPLITS_BALANCED, rc.SPLITS_LAST_ROUND):
             need = L.workspace_bytes(B, H, D, splits)
             st = _step(L, B=B, H=H, D=D, ts=ts, splits=splits, ws=FAKE if need else None, wsb=need, lse=FAKE)
             assert st == rc.RC_OK, (kinds, lens, splits, rc.lib().rc_last_error().decode())

@@ -101,7 +101,7 @@ int launch_attention(const Params& p, int D, void*) {
   check_params(p, D, false);
   REQUIRE(p.lr_tiles >= 0 && p.lr_tiles < kCUs, p.lr_tiles, 0);
   if (p.lr_tiles > 0) {
-    REQUIRE(p.splits == 2 && p.tail_num > 0 && !p.fp8 && p.cp.blocks == 0, p.splits, p.tail_num);
+    REQUIRE(p.splits == 2 && p.tail_num > 0 && p.cp.blocks == 0, p.splits, p.tail_num);
     REQUIRE(p.lr_tiles <= int64_t(p.B) * p.H * p.n_qtiles, p.lr_tiles, p.n_qtiles);
   }
   const CopyTail& c = p.cp;

@@ -142,7 +142,7 @@ def test_argument_errors_launch_nothing():
         assert rc.lib().rc_last_error().decode() != ""
     assert _prefill(L, kc=None) == A
     assert _step(L, vc=None) == A
-    assert _step(L, splits=-3) == A
+    assert _step(L, splits=-4) == A
     assert _step(L, splits=33) == A
     assert _step(L, splits=-2) == W                    # tail split, no workspace
     assert L.workspace_bytes(1, 2, 128, -2) == L.workspace_bytes(1, 2, 128, 2)
@@ -227,7 +227,10 @@ def test_auto_splits_and_workspace():
     assert L.auto_splits(1, 22, 128) == 1            # 198 tiles: 4 rounds on 58 CUs
     assert L.auto_splits(1, 21, 128) == rc.SPLITS_TAIL   # 189 tiles: 3 rounds on 67 CUs
     assert L.workspace_bytes(1, 21, 128, 0) == 2 * 21 * 4608 * 130 * 4
-    assert L.auto_splits(1, 29, 128) == 1            # 261 query tiles fill every CU
+    # more query tiles than CUs: the last round's tiles split on the idle CUs
+    assert L.auto_splits(1, 29, 128) == rc.SPLITS_LAST_ROUND   # 261 tiles: the last 5 over 251 idle CUs
+    assert L.workspace_bytes(1, 29, 128, 0) == 2 * 5 * 512 * 130 * 4
+    assert L.auto_splits(1, 56, 128) == 1            # 504 tiles: the last 248 on 8 idle CUs, not split
     assert L.auto_splits(1, 15, 128) == rc.SPLITS_TAIL   # 135 query tiles: more than half
     assert L.auto_splits(1, 14, 128) == 2            # 126 query tiles: two even splits keep one round
     # one GPU's share of 24 heads over 8: 27 query tiles, 9 splits keep one round
@@ -248,6 +251,15 @@ def test_step_launch_shape():
     assert L.launch_shape(1, 24, 128, rc.SPLITS_BALANCED) == (256, 256, rc.SPLITS_BALANCED)
     assert L.launch_shape(1, 24, 128, 3) == (648, 512, 3)
     assert L.launch_shape(2, 24, 128, 1) == (432, 512, 1)
+    # more query tiles than CUs: the last-round split (B = 2: 432 tiles, the
+    # last 176 as two pieces each; 32 heads: 288 tiles, the last 32 split);
+    # where it does not apply (one round) the step runs unsplit
+    assert L.launch_shape(2, 24, 128) == (432 + 176, 512, rc.SPLITS_LAST_ROUND)
+    assert L.launch_shape(1, 32, 128) == (288 + 32, 512, rc.SPLITS_LAST_ROUND)
+    assert L.launch_shape(1, 32, 128, rc.SPLITS_LAST_ROUND, fp8=True) == (320, 512, rc.SPLITS_LAST_ROUND)
+    assert L.launch_shape(1, 24, 128, rc.SPLITS_LAST_ROUND) == (216, 512, 1)
+    assert L.workspace_bytes(1, 32, 128, rc.SPLITS_LAST_ROUND) == 2 * 32 * 512 * 130 * 4
+    assert L.workspace_bytes(1, 24, 128, rc.SPLITS_LAST_ROUND) == 0
     # the FP8 step tiles its queries as the bf16 step does, and splits the same way
     assert L.launch_shape(1, 24, 128, 0, fp8=True) == (216, 512, 1)
     assert L.launch_shape(1, 24, 128, rc.SPLITS_TAIL, fp8=True) == (432, 512, 2)
@@ -256,7 +268,7 @@ def test_step_launch_shape():
     assert L.launch_shape(1, 15, 128, 0, fp8=True) == (270, 512, 2)
     # 7 heads: 63 tiles under the automatic choice of 4 even splits
     assert L.launch_shape(1, 7, 128, 0, fp8=True) == L.launch_shape(1, 7, 128) == (4 * 7 * 9, 512, 4)
-    for kw, status in ((dict(D=96), rc.RC_ERR_UNSUPPORTED), (dict(splits=-3), rc.RC_ERR_ARG),
+    for kw, status in ((dict(D=96), rc.RC_ERR_UNSUPPORTED), (dict(splits=-4), rc.RC_ERR_ARG),
                        (dict(splits=33), rc.RC_ERR_ARG), (dict(B=0), rc.RC_ERR_ARG),
                        (dict(splits=rc.SPLITS_BALANCED, fp8=True), rc.RC_ERR_UNSUPPORTED)):
         args = dict(B=1, H=2, D=128, splits=0, fp8=False)

@@ -117,6 +117,15 @@ def test_fp8_cfg_two_branch_batch():
     check_fp8_request(wl, "perref", every=113, splits=1)
 
 
+def test_fp8_last_round_split():
+    """More query tiles than CUs (32 heads: 288 tiles): the last round's tiles
+    as long and short pieces over the FP8 cache."""
+    wl = workload("ref5")
+    wl = Workload("ref5_h32_fp8", 1, 32, 128, wl.segments, seed=23)
+    assert rc.Layout(list(wl.segments), "perref").auto_splits(1, 32, 128) == rc.SPLITS_LAST_ROUND
+    check_fp8_request(wl, "perref", every=71, splits=0)
+
+
 def test_fp8_three_head_share_split_kv():
     wl = workload("ref5")
     wl = Workload("ref5_h3_fp8", 1, 3, 128, wl.segments, seed=19)

@@ -211,6 +211,38 @@ def test_full_recompute_last_round_split(name, segs, preset, B, H, D):
     check_lse(lse, ls2, f"{name} split rows", srows)
 
 
+# The step's last-round split (the automatic choice when the query tiles
+# outnumber the CUs): the 5-reference shape at 32 and 40 heads on sampled rows
+# (prefill and steps 0 and 39), a ragged layout element by element, B = 3.
+@pytest.mark.parametrize("H", [32, 40])
+def test_step_last_round_split_ref5_heads(H):
+    from synthgen import Workload
+    base = workload("ref5")
+    wl = Workload(f"ref5_h{H}", 1, H, base.D, base.segments, std=base.std, seed=13)
+    L = rc.Layout(list(wl.segments), "perref")
+    assert L.auto_splits(1, H, wl.D) == rc.SPLITS_LAST_ROUND
+    check_request(wl, "perref", every=67, splits=0, steps=(0, 39))
+    # the tiles outside the last round are computed whole: bit-equal to the unsplit step
+    inp = draw_inputs(wl)
+    _, _, kc, vc = run_prefill(L, inp, wl.scale, want_lse=False)
+    o_lr, _ = run_step(L, inp, kc, vc, wl.scale, splits=rc.SPLITS_LAST_ROUND, want_lse=False)
+    o_1, _ = run_step(L, inp, kc, vc, wl.scale, splits=1, want_lse=False)
+    torch.cuda.synchronize()
+    live_lens = [n for kd, n in wl.segments if kd in (1, 2)]
+    keep = ~last_round_rows(live_lens, 1, H)
+    assert torch.equal(o_lr[keep], o_1[keep])
+
+
+@pytest.mark.parametrize("B,H,D", [(1, 96, 64), (3, 32, 128)])
+def test_step_last_round_split_ragged(B, H, D):
+    from synthgen import Workload
+    segs = ((0, 40), (1, 100), (2, 900), (3, 700), (3, 333))
+    wl = Workload(f"lastround_step_B{B}_H{H}_D{D}", B, H, D, segs, std=1.0, seed=21)
+    L = rc.Layout(list(segs), "perref")
+    assert L.auto_splits(B, H, D) == rc.SPLITS_LAST_ROUND
+    check_request(wl, "perref", every=3, splits=rc.SPLITS_LAST_ROUND)
+
+
 def test_ref1_request_40_steps():
     """Single-reference 1024^2 shape: 1 prefill + 40 steps with fresh live
     Q/K/V each step, all run over the one cache.  Steps 0, 19 and 39 are

@@ -58,3 +58,18 @@ def test_noalloc_without_splits_and_over_limit():
         rc.step_masked_attention_noalloc(L, ql, kl, vl, kc, vc, o, splits=4, scale=wl.scale)
     assert e.value.status == rc.RC_ERR_WORKSPACE
     assert "scratch" in str(e.value)
+
+
+def test_noalloc_last_round_split():
+    """The last-round split through the static scratch: 32 heads at the
+    5-reference shape, then a smaller ragged grid that also splits."""
+    big = Workload("ref5_h32", 1, 32, 128, workload("ref5").segments, seed=25)
+    small = Workload("ragged_h96", 1, 96, 64, ((0, 40), (1, 100), (2, 900), (3, 700), (3, 333)), seed=27)
+    sizes = []
+    for wl in (big, small):
+        L, live, kc, vc = _prepare(wl)
+        need = L.workspace_bytes(wl.B, wl.H, wl.D, rc.SPLITS_LAST_ROUND)
+        assert 0 < need <= rc.NOALLOC_SCRATCH_BYTES
+        sizes.append(need)
+        _compare(wl, L, live, kc, vc, rc.SPLITS_LAST_ROUND)
+    assert sizes[1] < sizes[0]
