@@ -199,8 +199,9 @@ rc_status rc_step_launch_shape(const rc_layout* L, int32_t B, int32_t H, int32_t
  * *copy_rows the flat cache rows (b, h, row) [0, *copy_rows) that they
  * copy; the store kernel copies the other B * H * N_cached - *copy_rows rows
  * after the attention.  The copy work-groups run on the CUs that the
- * attention grid's partial last round leaves free, and take as many rows as
- * a dispatch model of that round says fit there.  Host only; RC_ERR_ARG on
+ * attention grid leaves free before it ends (its partial last round, and
+ * CUs whose work-groups end early), and take as many rows as a dispatch
+ * model of the grid says fit there.  Host only; RC_ERR_ARG on
  * bad arguments or null outputs, RC_ERR_MASK_NOT_CACHEABLE as the
  * prefill. */
 rc_status rc_prefill_launch_plan(const rc_layout* L, int32_t B, int32_t H, int32_t D, int64_t* attn_wgs,

@@ -268,8 +268,9 @@ bool per_batch_launches(const Params& p) {
 // i mod 8 and there, in order, to the first of the XCD's 32 CUs to become
 // free; a work-group lasts its query tile's key tiles plus kTileOverhead
 // tile times.  The copy work-groups come after the last attention
-// work-group, at most one on each CU the partial last round leaves free,
-// and may run until the attention ends: a CU copies about kCopyRowsPerTile cache rows
+// work-group, at most one on each CU that becomes free before the attention
+// ends (short work-groups, such as one-key-tile anchor rows, free theirs
+// early), and may run until the attention ends: a CU copies about kCopyRowsPerTile cache rows
 // (K and V of one token and head) per tile time (measured: about 100 at
 // D = 128, 512-row tiles).  The model stops at kMaxModelWGs work-groups,
 // where the store is a small part of the launch.
@@ -286,8 +287,10 @@ CopyPlan plan_copy_tail(const Params& p, int64_t n_cached) {
   const int64_t R = int64_t(p.B) * p.H * n_cached;
   if (R >= (int64_t(1) << 31)) return none;  // the copy work-groups index rows in 32 bits
   const int64_t A = per_batch_launches(p) ? int64_t(p.H) * p.n_qtiles : int64_t(p.B) * p.H * p.n_qtiles;
-  if (A <= 0 || A > kMaxModelWGs || A % kCUs == 0) return none;
-  const int64_t C = kCUs - A % kCUs;
+  if (A <= 0 || A > kMaxModelWGs) return none;
+  // candidates: one copy work-group per CU, placed in dispatch order; the
+  // ones the model sees start only when the attention ends drop out below
+  const int64_t C = kCUs;
   constexpr int kXcds = 8, kPerXcd = kCUs / kXcds;
   typedef std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> FreeAt;
   std::vector<FreeAt> cu(kXcds);
@@ -311,8 +314,8 @@ CopyPlan plan_copy_tail(const Params& p, int64_t n_cached) {
   }
   // Copy work-groups take equal row counts, so the one with the shortest
   // window sets the pace: keep the first c of them (those placed earliest)
-  // with the largest c x (shortest window among them), and no more than
-  // give each kCopyMinRows rows.
+  // with the largest c x (shortest window among them), no more than give
+  // each kCopyMinRows rows, and no more than take every row.
   std::vector<int64_t> win(static_cast<size_t>(C), 0);
   int64_t window = end, best_c = 0;
   for (int64_t j = 0; j < C; ++j) {
@@ -322,8 +325,15 @@ CopyPlan plan_copy_tail(const Params& p, int64_t n_cached) {
     win[size_t(j)] = window;
     if ((j + 1) * window > (best_c ? best_c * win[size_t(best_c - 1)] : 0)) best_c = j + 1;
   }
-  const int64_t c = std::min(best_c, R / kCopyMinRows);
+  int64_t c = std::min(best_c, R / kCopyMinRows);
   if (c <= 0) return none;
+  // When they can take every row, as few as can: each busy CU lowers the
+  // clock of the attention work-groups still running.
+  if (c * kCopyRowsPerTile * win[size_t(c - 1)] >= R) {
+    int64_t m = 1;
+    while (m < c && m * kCopyRowsPerTile * win[size_t(m - 1)] < R) ++m;
+    c = m;
+  }
   const int64_t rows = std::min(R, c * kCopyRowsPerTile * win[size_t(c - 1)]);
   return CopyPlan{int32_t(c), rows};
 }

@@ -105,7 +105,7 @@ int launch_attention(const Params& p, int D, void*) {
     REQUIRE(p.lr_tiles <= int64_t(p.B) * p.H * p.n_qtiles, p.lr_tiles, p.n_qtiles);
   }
   const CopyTail& c = p.cp;
-  REQUIRE(c.blocks >= 0 && c.blocks < kCUs, c.blocks, 0);
+  REQUIRE(c.blocks >= 0 && c.blocks <= kCUs, c.blocks, 0);
   if (c.blocks > 0) {
     REQUIRE(p.splits == 1 && !p.fp8, p.splits, p.fp8);
     REQUIRE(c.k_src && c.v_src && c.k_dst && c.v_dst, 0, 0);

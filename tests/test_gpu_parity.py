@@ -125,7 +125,11 @@ CACHE_STORE = [
     ("split_ragged", RAGGED5, "perref", 3, 29, 128, "split"),
     ("split_per_batch", RAGGED5, "perref", 2, 64, 64, "split"),
     ("split_paper", RAGGED5, "paper", 1, 72, 64, "split"),
-    ("store_only", [(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "perref", 2, 32, 64, "store"),
+    # 256 equal work-groups (under the paper mask every static tile reads all static keys)
+    ("store_only", [(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "paper", 2, 32, 64, "store"),
+    # the same layout under the per-reference mask: the one-key-tile anchor work-groups free their CUs
+    ("split_anchor_cus", [(0, 64), (1, 64), (2, 256), (3, 256), (3, 256), (3, 256)], "perref", 2, 32, 64,
+     "split"),
     ("split_32_segments", MANY, "perref", 1, 13, 128, "split"),
 ]
 
