@@ -360,6 +360,106 @@ def test_prefill_launch_plan():
                                            None) == rc.RC_ERR_ARG
 
 
+def _tiles(kinds, lens, vis, rows, keys, bm=512):
+    """Key tiles of each query tile, in the kernel's per-head tile order:
+    query segments `rows` in sequence order, tiles of bm rows inside each; a
+    segment's visible key segments merged into runs that are adjacent in the
+    key buffer (the segments `keys`, in sequence order), 64 keys per tile."""
+    pos, p = {}, 0
+    for i in keys:
+        pos[i] = p
+        p += lens[i]
+    out = []
+    for q in rows:
+        runs = []
+        for k in range(len(kinds)):
+            if not vis[q][k]:
+                continue
+            if runs and runs[-1][0] + runs[-1][1] == pos[k]:
+                runs[-1][1] += lens[k]
+            else:
+                runs.append([pos[k], lens[k]])
+        out += [sum(-(-n // 64) for _, n in runs)] * (-(-lens[q] // bm))
+    return out
+
+
+def _model_copy_plan(kinds, lens, vis, B, H):
+    """The prefill's copy plan as the header documents it, written out: a
+    dispatch model of the attention grid (work-group i to XCD i mod 8, there
+    to the first of 32 CUs to free; key tiles + 2 tile times each), up to 256
+    copy work-groups after it, the first c with the largest c x (shortest
+    window), at least 64 rows each, 64 rows per tile time, and the fewest that
+    take every row when they can."""
+    import heapq
+    static = [i for i, k in enumerate(kinds) if k in (0, 3)]
+    tiles = _tiles(kinds, lens, vis, static, static)
+    nt = len(tiles)
+    R = B * H * sum(lens[i] for i in om.cached_segments(kinds, vis))
+    A = H * nt if (B > 1 and 2 * H * nt > 256) else B * H * nt
+    if R <= 0 or R >= 2 ** 31 or A <= 0 or A > 65536:
+        return 0, 0
+    heaps = [[0] * 32 for _ in range(8)]
+    per, rem, end = A >> 3, A & 7, 0
+    for bid in range(A):
+        x, kx = bid & 7, bid >> 3
+        w = x * (per + 1) + kx if x < rem else rem * (per + 1) + (x - rem) * per + kx
+        fin = heapq.heappop(heaps[x]) + tiles[w % nt] + 2
+        heapq.heappush(heaps[x], fin)
+        end = max(end, fin)
+    win, window, best = [], end, 0
+    for j in range(256):
+        window = min(window, end - heapq.heappop(heaps[(A + j) & 7]))
+        win.append(window)
+        if (j + 1) * window > (best * win[best - 1] if best else 0):
+            best = j + 1
+    c = min(best, R // 64)
+    if c <= 0:
+        return 0, 0
+    if c * 64 * win[c - 1] >= R:
+        c = next(m for m in range(1, c + 1) if m * 64 * win[m - 1] >= R)
+    return c, min(R, c * 64 * win[c - 1])
+
+
+def _model_last_round(kinds, lens, vis, B, H):
+    """The full recompute's last-round split as documented: T = A mod 256 of
+    A > 256 whole tiles, R = ceil(T / (256 - T)) <= 3 rounds of short pieces,
+    every split tile >= 16 key tiles."""
+    every = list(range(len(kinds)))
+    tiles = _tiles(kinds, lens, vis, every, every)
+    nt = len(tiles)
+    A = B * H * nt
+    T = A % 256
+    if A <= 256 or T == 0 or -(-T // (256 - T)) > 3:
+        return 0
+    if any(tiles[w % nt] < 16 for w in range(A - T, A)):
+        return 0
+    return T
+
+
+def test_launch_plans_match_their_documented_models():
+    """The prefill's copy plan and the full recompute's last-round split
+    against their models written out in Python, over random layouts, mask
+    presets, batch sizes and head counts (grids from one work-group to many
+    rounds)."""
+    rng = random.Random(23)
+    n_copy = n_split = 0
+    for _ in range(150):
+        kinds, lens = random_layout(rng)
+        preset = rng.choice(["paper", "perref", "isolated", "dense"])
+        L = rc.Layout(list(zip(kinds, lens)), preset)
+        vis = L.visible
+        B, H = rng.choice([1, 2, 3]), rng.choice([1, 2, 5, 24, 40, 96])
+        T = _model_last_round(kinds, lens, vis, B, H)
+        assert L.full_workspace_bytes(B, H, 128) == 2 * T * 512 * 130 * 4, (kinds, lens, preset, B, H)
+        n_split += T > 0
+        if not om.is_cacheable(kinds, om.PRESETS[preset](kinds)) or L.rows(rc.ROWS_STATIC) == 0:
+            continue
+        _, c, r = L.prefill_plan(B, H, 128)
+        assert (c, r) == _model_copy_plan(kinds, lens, vis, B, H), (kinds, lens, preset, B, H)
+        n_copy += c > 0
+    assert n_copy > 20 and n_split > 5, (n_copy, n_split)
+
+
 def test_binding_checks_row_counts():
     """Every read and write is sized from the layout's row count, so the
     binding refuses Q with another token count before anything else (no GPU
