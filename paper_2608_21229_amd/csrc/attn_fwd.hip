@@ -1251,9 +1251,14 @@ __device__ __forceinline__ void copy_tail(const CopyTail& c, int j, int tid) {
       if (r < r1) {
         const uint32_t bh = r / uint32_t(c.n_cached), drow = r - bh * uint32_t(c.n_cached);
         const uint32_t b = bh / H, h = bh - b * H;
-        int si = 0;
-        while (si + 1 < c.n_copy && uint32_t(c.seg[si + 1].dst_row0) <= drow) ++si;
-        const int64_t srow = int64_t(c.seg[si].src_row0) + int64_t(drow) - c.seg[si].dst_row0;
+        // the run holding drow, by a loop over the whole table: its index is
+        // wave-uniform, so the table comes in through scalar loads (a per-lane
+        // index would read it with vector loads, whose waits also wait for the
+        // copy loads already in flight)
+        int64_t delta = 0;
+        for (int k = 0; k < c.n_copy; ++k)
+          if (drow >= uint32_t(c.seg[k].dst_row0)) delta = int64_t(c.seg[k].src_row0) - c.seg[k].dst_row0;
+        const int64_t srow = int64_t(drow) + delta;
         const int64_t so = int64_t(b) * c.src_sb + srow * c.src_st + int64_t(h) * D + g8;
         kx[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(c.k_src + so));
         vx[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(c.v_src + so));
