@@ -1531,9 +1531,10 @@ __global__ __launch_bounds__(256) void cache_store_kernel(const CacheStoreParams
   const int drow = int(rest % c.total_rows);
   rest /= c.total_rows;
   const int h = int(rest % c.H), b = int(rest / c.H);
-  int si = 0;
-  while (si + 1 < c.n_copy && c.seg[si + 1].dst_row0 <= drow) ++si;
-  const int srow = c.seg[si].src_row0 + (drow - c.seg[si].dst_row0);
+  int delta = 0;  // uniform loop over the run table: scalar loads
+  for (int k = 0; k < c.n_copy; ++k)
+    if (drow >= c.seg[k].dst_row0) delta = c.seg[k].src_row0 - c.seg[k].dst_row0;
+  const int srow = drow + delta;
   const int64_t so = int64_t(b) * c.src_sb + int64_t(srow) * c.src_st + int64_t(h) * c.D + g * 8;
   const int64_t dof = ((int64_t(b) * c.H + h) * c.n_cached + drow) * c.D + g * 8;
   *reinterpret_cast<u32x4*>(c.k_dst + dof) = *reinterpret_cast<const u32x4*>(c.k_src + so);

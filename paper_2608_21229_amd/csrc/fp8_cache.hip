@@ -36,11 +36,15 @@ __device__ __forceinline__ int fp8_exponent(float amax) {
   return m <= 0.875f ? k - 9 : k - 8;
 }
 
-// Source row (in the static buffers) of cache position pos.
+// Source row (in the static buffers) of cache position pos: a loop over the
+// whole run table with a wave-uniform index, so the table comes in through
+// scalar loads (a per-lane index would read it with vector loads, whose
+// waits also wait for the data loads in flight).
 __device__ __forceinline__ int source_row(const CacheStore8Params& c, int pos) {
-  int i = 0;
-  while (i + 1 < c.n_copy && pos >= c.seg[i + 1].dst_row0) ++i;
-  return c.seg[i].src_row0 + (pos - c.seg[i].dst_row0);
+  int delta = 0;
+  for (int k = 0; k < c.n_copy; ++k)
+    if (pos >= c.seg[k].dst_row0) delta = c.seg[k].src_row0 - c.seg[k].dst_row0;
+  return pos + delta;
 }
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
