@@ -270,10 +270,12 @@ bool per_batch_launches(const Params& p) {
 // tile times.  The copy work-groups come after the last attention
 // work-group, at most one on each CU that becomes free before the attention
 // ends (short work-groups, such as one-key-tile anchor rows, free theirs
-// early), and may run until the attention ends: a CU copies about kCopyRowsPerTile cache rows
-// (K and V of one token and head) per tile time (measured: about 100 at
-// D = 128, 512-row tiles).  The model stops at kMaxModelWGs work-groups,
-// where the store is a small part of the launch.
+// early), and may run until the attention ends, each counted on for
+// kCopyRowsPerTile cache rows (K and V of one token and head) per tile time:
+// a conservative figure (a copy work-group next to the attention measured
+// 100 or more at D = 128 with 512-row tiles, and larger settings were no
+// better overall).  The model stops at kMaxModelWGs work-groups, where the
+// store is a small part of the launch.
 namespace {
 constexpr int64_t kCopyRowsPerTile = 64;
 constexpr int64_t kTileOverhead = 2;
